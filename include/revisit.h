@@ -1,0 +1,200 @@
+/*
+ * revisit.h -- C interface of librevisit, the GPU (gfx950) hot path of
+ * training-free revisit consistency for autoregressive generative rendering
+ * (arXiv 2607.21848: pose-retrieved loop-closure memory, Sec. 4.2, and the
+ * geometric correspondence attention prior, Sec. 4.3).
+ *
+ * Three stages, one entry point each:
+ *
+ *   retrieve_chunks           -- pose retrieval over the history bank
+ *                                (Sec. 4.2, Eq. retrieval)
+ *   reproject_correspondence  -- per-token depth/pose reprojection into the
+ *                                retrieved frames with the occlusion test
+ *                                (Sec. 4.3, Eq. reprojection, Eq. visibility)
+ *   biased_chunk_attention    -- chunk attention with the Gaussian
+ *                                correspondence bias fused in
+ *                                (Sec. 4.3, Eq. bias)
+ *
+ * Conventions common to all entry points
+ * --------------------------------------
+ * - Every array argument is a DEVICE pointer owned by the caller and must
+ *   stay valid until the work queued on `stream` has completed. Outputs must
+ *   not alias inputs. The library allocates no memory and keeps no state
+ *   other than a per-thread last-error string.
+ * - Calls are asynchronous on `stream` (NULL = the default stream).
+ * - Arguments are validated on the host before anything is queued: on a
+ *   non-zero status nothing has been enqueued and rc_last_error() says why.
+ *   Device-resident index arrays (slots, selections) cannot be checked from
+ *   the host; out-of-range entries there are given a defined meaning below
+ *   instead of being read out of bounds.
+ * - No C++ exception crosses this interface.
+ * - Poses are row-major 4x4 camera-to-world matrices [R | c; 0 0 0 1]
+ *   (Sec. 4.1: camera-to-world rotation and centre), camera axes x right,
+ *   y down, z forward; planar depth is the camera-frame z (Sec. 4.1).
+ * - Intrinsics are (fx, fy, cx, cy) in depth-map pixel units, pixel (x, y)
+ *   covering [x, x+1) x [y, y+1). A token is a p x p block of depth pixels;
+ *   the token-grid intrinsics of Sec. 4.1 are these divided by p.
+ */
+#ifndef REVISIT_H
+#define REVISIT_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+    REVISIT_OK = 0,
+    REVISIT_ERR_NULL = 1,        /* a required pointer is NULL */
+    REVISIT_ERR_SHAPE = 2,       /* a size is negative, inconsistent or too large */
+    REVISIT_ERR_UNSUPPORTED = 3, /* dtype / head dimension not built */
+    REVISIT_ERR_PARAM = 4,       /* a method parameter is out of its domain */
+    REVISIT_ERR_LAUNCH = 5       /* the HIP runtime refused the launch */
+};
+
+/* Element types of biased_chunk_attention. */
+enum { REVISIT_BF16 = 1, REVISIT_F32 = 2 };
+
+/* Correspondence reason codes written to out_idx by reproject_correspondence
+ * (the rejection causes of Sec. 4.3, design choice (iii), plus an empty
+ * retrieved slot). A value >= 0 is a key index within the source frame. */
+enum {
+    REVISIT_UNDEFINED = -1, /* query depth not finite or <= 0 */
+    REVISIT_BEHIND = -2,    /* [X_s]_z <= 0 */
+    REVISIT_OFF_GRID = -3,  /* u^ outside [0, w) x [0, h) */
+    REVISIT_OCCLUDED = -4,  /* Eq. visibility fails (or source depth NaN) */
+    REVISIT_NO_SOURCE = -5  /* the retrieved slot is empty */
+};
+
+/* Largest k accepted by retrieve_chunks. */
+#define REVISIT_MAX_K 32
+
+/* Human-readable name of a status code (static string). */
+const char* rc_status_string(int status);
+
+/* Detail of the last non-zero status returned on the calling thread
+ * (static per-thread buffer, overwritten by the next failing call). */
+const char* rc_last_error(void);
+
+/*
+ * retrieve_chunks -- Sec. 4.2, Eq. retrieval.
+ *
+ * For each query chunk q with pose query_c2w[q] and chunk index
+ * n = query_chunk[q], score every bank entry j (entry j IS chunk j):
+ *     s(j) = |c_j - c_n| / E + w_v (1 - v_j . v_n)
+ * with c = last column of the pose and v = R e_z (third column, used as
+ * stored), keep j if j >= first_candidate, n - j >= delta,
+ * |c_j - c_n| / E <= tau_c and v_j . v_n >= cos(tau_v), and return the k
+ * admissible entries of smallest score, ties broken by smaller j. Scores
+ * are evaluated in double precision; cos(tau_v) is evaluated once on the
+ * host.
+ *
+ *   bank_c2w      [n_bank][4][4] fp32   one representative pose per chunk
+ *   query_c2w     [n_query][4][4] fp32
+ *   query_chunk   [n_query] int32       n of each query
+ *   E > 0, w_v, tau_c, tau_v (radians): finite
+ *   k             1..REVISIT_MAX_K
+ *   out_idx       [n_query][k] int32    chunk ids, -1 past the count
+ *   out_score     [n_query][k] fp32     nullable; s rounded to fp32, +inf past the count
+ *   out_count     [n_query] int32       number of admissible entries returned (0..k);
+ *                                       count < k means the retrieved slot
+ *                                       extends the recent window (Sec. 4.2)
+ *   frames_per_chunk, out_frame_sel  nullable [n_query][k * frames_per_chunk]:
+ *                 entry i*F + f = out_idx[i]*F + f, or -1 past the count; this
+ *                 is the source-frame selection reproject_correspondence takes.
+ *
+ * n_bank == 0 or n_query == 0 is valid (count 0 / nothing to do).
+ */
+int retrieve_chunks(const float* bank_c2w, int32_t n_bank,
+                    const float* query_c2w, const int32_t* query_chunk, int32_t n_query,
+                    float E, float w_v, float tau_c, float tau_v,
+                    int32_t delta, int32_t first_candidate, int32_t k,
+                    int32_t* out_idx, float* out_score, int32_t* out_count,
+                    int32_t frames_per_chunk, int32_t* out_frame_sel,
+                    hipStream_t stream);
+
+/*
+ * reproject_correspondence -- Sec. 4.3, Eq. reprojection and Eq. visibility.
+ *
+ * For B independent problems, every token p of every target frame t and every
+ * source frame s:
+ *     z_p  = mean of the token's p x p depth pixels (row-major sum)
+ *     X_t  = z_p K_t^-1 u~_p,   u_p = (col + 1/2, row + 1/2) token units
+ *     X_s  = R_s^T (R_t X_t + c_t - c_s)
+ *     u^   = pi(K_s X_s)
+ * accepted iff 0 <= u^_x < w, 0 <= u^_y < h and
+ *     [X_s]_z <= (1 + eps) D_s(u^),   D_s = pooled depth of the cell holding u^.
+ * All arithmetic is IEEE double in exactly this order (no contraction), so the
+ * results are reproducible bit for bit on any IEEE host.
+ *
+ *   tgt_depth [B][Tq][h*p][w*p] fp32, tgt_c2w [B][Tq][4][4], tgt_K [B][Tq][4]
+ *   sources, either
+ *     src_sel == NULL: src_depth [B][S][h*p][w*p], src_c2w [B][S][4][4],
+ *                      src_K [B][S][4] (n_src ignored), or
+ *     src_sel != NULL: a frame bank src_depth [n_src][h*p][w*p], src_c2w
+ *                      [n_src][4][4], src_K [n_src][4] shared by all problems,
+ *                      and src_sel [B][S] int32 choosing the frame of each slot;
+ *                      an entry outside [0, n_src) means "no source" and the
+ *                      whole slot is written as REVISIT_NO_SOURCE.
+ *   p >= 1 latent pixels per token side; eps >= 0 finite.
+ *   out_uv  [B][S][Tq*h*w][2] fp32: u^ in token units (row-major token order,
+ *           target frames outer); NaN for UNDEFINED, BEHIND and NO_SOURCE.
+ *   out_idx [B][S][Tq*h*w] int32: key index floor(u^_y) w + floor(u^_x) within
+ *           the source frame, or a negative REVISIT_* reason code.
+ *
+ * Any of B, Tq, S equal to 0 is valid (nothing to do). out_uv must be 8-byte
+ * aligned (REVISIT_ERR_SHAPE otherwise).
+ */
+int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const float* tgt_K,
+                             const float* src_depth, const float* src_c2w, const float* src_K,
+                             const int32_t* src_sel, int32_t n_src,
+                             int32_t B, int32_t Tq, int32_t S, int32_t h, int32_t w, int32_t p,
+                             float eps,
+                             float* out_uv, int32_t* out_idx,
+                             hipStream_t stream);
+
+/*
+ * biased_chunk_attention -- Sec. 4.3, Eq. bias and design choices (ii)-(iii).
+ *
+ * Per head, with no mask (every query sees all Lk keys):
+ *     A_pk = softmax_scale * q_p . k_k + lambda * B_s(p, k)
+ *     B_s(p, k) = -|u_k - u^_s(p)|^2 / (2 sigma^2)
+ *     O = softmax_k(A) V,   LSE_p = log sum_k exp(A_pk)  (natural log)
+ * The bias applies only to key columns of KV frames whose slot is a retrieved
+ * frame s in [0, S), and only for queries with corr_idx[s][p] >= 0; every
+ * other logit is the plain scaled dot product. u_k = (k_x + 1/2, k_y + 1/2)
+ * with (k_y, k_x) = divmod(k mod (h w), w). The bias is computed on the fly
+ * from the correspondence map, never materialised.
+ *
+ *   dtype       REVISIT_BF16 (D = 128) or REVISIT_F32 (D = 64 or 128)
+ *   q           [Lq][H][D], k, v [Lk][H][D], o [Lq][H][D] in dtype
+ *               (fp32 accumulation and softmax in both cases)
+ *   lse         nullable [H][Lq] fp32
+ *   Lq >= 0, Lk >= 1, Lk % (h*w) == 0, Lk / (h*w) <= 4096 KV frames
+ *   kv_frame_slot [Lk/(h*w)] int32: s in [0, S) for a retrieved frame, any
+ *               other value = unbiased (anchor / recent / current frames)
+ *   corr_uv     [S][Lq][2] fp32, corr_idx [S][Lq] int32 (reproject_correspondence
+ *               output for this chunk's Lq query tokens); S == 0 or
+ *               lambda == 0 turns the bias off (pointers may then be NULL)
+ *   softmax_scale > 0 (normally 1/sqrt(D)), sigma > 0, lambda finite.
+ *   q, k, v, o must be 16-byte aligned and corr_uv 8-byte aligned
+ *   (REVISIT_ERR_SHAPE otherwise).
+ *
+ * Lq == 0 is valid (nothing to do).
+ */
+int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
+                           float* lse, int32_t dtype,
+                           int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
+                           const int32_t* kv_frame_slot,
+                           const float* corr_uv, const int32_t* corr_idx, int32_t S,
+                           float softmax_scale, float lambda, float sigma,
+                           hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REVISIT_H */

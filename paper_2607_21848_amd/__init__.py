@@ -1,0 +1,174 @@
+"""MI355X (gfx950) hot path of training-free revisit consistency
+(arXiv 2607.21848, Sec. 4.2 and Sec. 4.3).
+
+Python binding of librevisit: argument marshalling only. Every stage runs
+in the library's HIP kernels; torch tensors supply device memory and the
+current HIP stream. The three entry points mirror include/revisit.h:
+
+* ``retrieve_chunks``          -- pose retrieval (Sec. 4.2, Eq. retrieval)
+* ``reproject_correspondence`` -- depth/pose reprojection and visibility
+                                  (Sec. 4.3, Eq. reprojection, Eq. visibility)
+* ``biased_chunk_attention``   -- attention with the Gaussian correspondence
+                                  bias (Sec. 4.3, Eq. bias)
+
+Each accepts optional preallocated outputs (``out=``) so a caller can run
+the path without allocating.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Sequence
+
+import torch
+
+from . import _lib
+from ._lib import BF16, F32, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
+
+__all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "RevisitError", "lib"]
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape: Optional[Sequence[int]] = None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device}); there is no CPU path")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def retrieve_chunks(bank_c2w: torch.Tensor, query_c2w: torch.Tensor, query_chunk: torch.Tensor, *,
+                    E: float, w_v: float, tau_c: float, tau_v: float, delta: int, first_candidate: int, k: int,
+                    frames_per_chunk: Optional[int] = None, out=None):
+    """Top-k pose retrieval. bank_c2w [N,4,4] f32, query_c2w [Q,4,4] f32,
+    query_chunk [Q] i32. Returns (idx [Q,k] i32, score [Q,k] f32,
+    count [Q] i32, frame_sel [Q,k*F] i32 or None)."""
+    dev = query_c2w.device
+    N, Q = bank_c2w.shape[0], query_c2w.shape[0]
+    _need(bank_c2w, "bank_c2w", torch.float32, (N, 4, 4), dev)
+    _need(query_c2w, "query_c2w", torch.float32, (Q, 4, 4), dev)
+    _need(query_chunk, "query_chunk", torch.int32, (Q,), dev)
+    if out is None:
+        idx = torch.empty((Q, k), dtype=torch.int32, device=dev)
+        score = torch.empty((Q, k), dtype=torch.float32, device=dev)
+        count = torch.empty((Q,), dtype=torch.int32, device=dev)
+        sel = (torch.empty((Q, k * frames_per_chunk), dtype=torch.int32, device=dev)
+               if frames_per_chunk is not None else None)
+    else:
+        idx, score, count, sel = out
+    st = lib().retrieve_chunks(_ptr(bank_c2w), N, _ptr(query_c2w), _ptr(query_chunk), Q, E, w_v, tau_c, tau_v,
+                               delta, first_candidate, k, _ptr(idx), _ptr(score), _ptr(count),
+                               frames_per_chunk or 0, _ptr(sel), _stream(dev))
+    _lib.check("retrieve_chunks", st)
+    return idx, score, count, sel
+
+
+def reproject_correspondence(tgt_depth: torch.Tensor, tgt_c2w: torch.Tensor, tgt_K: torch.Tensor,
+                             src_depth: torch.Tensor, src_c2w: torch.Tensor, src_K: torch.Tensor, *,
+                             p: int, eps: float, src_sel: Optional[torch.Tensor] = None, out=None):
+    """Correspondence of every target token into every source frame.
+
+    Batched: tgt_depth [B,Tq,h*p,w*p], tgt_c2w [B,Tq,4,4], tgt_K [B,Tq,4];
+    sources [B,S,...] or, with src_sel [B,S] i32, a frame bank [n_src,...].
+    Unbatched inputs (no leading B) give unbatched outputs.
+    Returns (uv [B,S,Tq*h*w,2] f32, idx [B,S,Tq*h*w] i32)."""
+    batched = tgt_depth.dim() == 4
+    if not batched:
+        tgt_depth, tgt_c2w, tgt_K = tgt_depth[None], tgt_c2w[None], tgt_K[None]
+        if src_sel is None:
+            src_depth, src_c2w, src_K = src_depth[None], src_c2w[None], src_K[None]
+        else:
+            src_sel = src_sel[None]
+    dev = tgt_depth.device
+    B, Tq, Hd, Wd = tgt_depth.shape
+    if Hd % p or Wd % p:
+        raise ValueError(f"depth map {Hd}x{Wd} is not a whole number of {p}x{p} tokens")
+    h, w = Hd // p, Wd // p
+    _need(tgt_depth, "tgt_depth", torch.float32, None, dev)
+    _need(tgt_c2w, "tgt_c2w", torch.float32, (B, Tq, 4, 4), dev)
+    _need(tgt_K, "tgt_K", torch.float32, (B, Tq, 4), dev)
+    if src_sel is None:
+        S = src_depth.shape[1]
+        _need(src_depth, "src_depth", torch.float32, (B, S, Hd, Wd), dev)
+        _need(src_c2w, "src_c2w", torch.float32, (B, S, 4, 4), dev)
+        _need(src_K, "src_K", torch.float32, (B, S, 4), dev)
+        n_src = 0
+    else:
+        S = src_sel.shape[1]
+        n_src = src_depth.shape[0]
+        _need(src_sel, "src_sel", torch.int32, (B, S), dev)
+        _need(src_depth, "src_depth", torch.float32, (n_src, Hd, Wd), dev)
+        _need(src_c2w, "src_c2w", torch.float32, (n_src, 4, 4), dev)
+        _need(src_K, "src_K", torch.float32, (n_src, 4), dev)
+    Lq = Tq * h * w
+    if out is None:
+        uv = torch.empty((B, S, Lq, 2), dtype=torch.float32, device=dev)
+        idx = torch.empty((B, S, Lq), dtype=torch.int32, device=dev)
+    else:
+        uv, idx = out
+        _need(uv, "out uv", torch.float32, (B, S, Lq, 2), dev)
+        _need(idx, "out idx", torch.int32, (B, S, Lq), dev)
+    st = lib().reproject_correspondence(_ptr(tgt_depth), _ptr(tgt_c2w), _ptr(tgt_K), _ptr(src_depth),
+                                        _ptr(src_c2w), _ptr(src_K), _ptr(src_sel), n_src, B, Tq, S, h, w, p,
+                                        eps, _ptr(uv), _ptr(idx), _stream(dev))
+    _lib.check("reproject_correspondence", st)
+    if not batched:
+        return uv[0], idx[0]
+    return uv, idx
+
+
+def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv_frame_slot: torch.Tensor,
+                           corr_uv: Optional[torch.Tensor], corr_idx: Optional[torch.Tensor], *,
+                           h: int, w: int, softmax_scale: float, lam: float, sigma: float,
+                           return_lse: bool = True, out=None):
+    """Attention with the Gaussian correspondence bias on retrieved-frame keys.
+
+    q [Lq,H,D], k, v [Lk,H,D] (bf16 with D=128, or fp32 with D in {64,128});
+    kv_frame_slot [Lk/(h*w)] i32; corr_uv [S,Lq,2] f32 and corr_idx [S,Lq] i32
+    (None = no bias). Returns (o [Lq,H,D], lse [H,Lq] f32 or None)."""
+    dev = q.device
+    Lq, H, D = q.shape
+    Lk = k.shape[0]
+    if q.dtype == torch.bfloat16:
+        dt = BF16
+    elif q.dtype == torch.float32:
+        dt = F32
+    else:
+        raise TypeError(f"q must be bfloat16 or float32 (got {q.dtype})")
+    _need(q, "q", q.dtype, None, dev)
+    _need(k, "k", q.dtype, (Lk, H, D), dev)
+    _need(v, "v", q.dtype, (Lk, H, D), dev)
+    _need(kv_frame_slot, "kv_frame_slot", torch.int32, None, dev)
+    S = 0
+    if corr_uv is not None:
+        S = corr_uv.shape[0]
+        _need(corr_uv, "corr_uv", torch.float32, (S, Lq, 2), dev)
+        _need(corr_idx, "corr_idx", torch.int32, (S, Lq), dev)
+    if out is None:
+        o = torch.empty_like(q)
+        lse = torch.empty((H, Lq), dtype=torch.float32, device=dev) if return_lse else None
+    else:
+        o, lse = out
+        _need(o, "o", q.dtype, (Lq, H, D), dev)
+        if lse is not None:
+            _need(lse, "lse", torch.float32, (H, Lq), dev)
+    st = lib().biased_chunk_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), dt, Lq, Lk, H, D, h, w,
+                                      _ptr(kv_frame_slot), _ptr(corr_uv), _ptr(corr_idx), S,
+                                      softmax_scale, lam, sigma, _stream(dev))
+    _lib.check("biased_chunk_attention", st)
+    return o, lse

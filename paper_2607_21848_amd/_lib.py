@@ -1,0 +1,67 @@
+"""ctypes loader for librevisit.so (the C interface in include/revisit.h).
+
+The library is built in-tree by ``paper_2607_21848_amd.build``. There is no
+fallback: if the shared library is missing or fails to load, every entry
+point raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_LIB = None
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librevisit.so")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH = 0, 1, 2, 3, 4, 5
+BF16, F32 = 1, 2
+MAX_K = 32
+EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
+            "biased_chunk_attention")
+
+_p = ctypes.c_void_p
+_i = ctypes.c_int32
+_f = ctypes.c_float
+
+
+class RevisitError(RuntimeError):
+    def __init__(self, fn: str, status: int, detail: str):
+        super().__init__(f"{fn}: status {status} ({status_string(status)}): {detail}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (loaded once)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"librevisit.so not found at {LIB_PATH}: build it with "
+                               "`python -m paper_2607_21848_amd.build` (there is no CPU fallback)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.rc_status_string.restype = ctypes.c_char_p
+        L.rc_status_string.argtypes = [ctypes.c_int]
+        L.rc_last_error.restype = ctypes.c_char_p
+        L.rc_last_error.argtypes = []
+        L.retrieve_chunks.restype = ctypes.c_int
+        L.retrieve_chunks.argtypes = [_p, _i, _p, _p, _i, _f, _f, _f, _f, _i, _i, _i, _p, _p, _p, _i, _p, _p]
+        L.reproject_correspondence.restype = ctypes.c_int
+        L.reproject_correspondence.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _f,
+                                               _p, _p, _p]
+        L.biased_chunk_attention.restype = ctypes.c_int
+        L.biased_chunk_attention.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _i,
+                                             _f, _f, _f, _p]
+        _LIB = L
+    return _LIB
+
+
+def status_string(status: int) -> str:
+    return lib().rc_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return lib().rc_last_error().decode()
+
+
+def check(fn: str, status: int) -> None:
+    if status != OK:
+        raise RevisitError(fn, status, last_error())

@@ -1,0 +1,190 @@
+// C entry points of librevisit: argument validation on the host, then one
+// kernel launch each on the caller's stream. Nothing is allocated; the only
+// state is a per-thread last-error string.
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/revisit.h"
+#include "internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int launched(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(REVISIT_ERR_LAUNCH, "%s: launch failed: %s", what, hipGetErrorString(e));
+    return REVISIT_OK;
+}
+
+bool finite(float x) { return isfinite(x); }
+
+bool aligned(const void* ptr, uintptr_t bytes) { return ((uintptr_t)ptr % bytes) == 0; }
+
+constexpr int64_t kMaxElems = (int64_t)1 << 40;
+constexpr int kMaxFrames = 4096;
+
+}  // namespace
+
+extern "C" {
+
+const char* rc_status_string(int status) {
+    switch (status) {
+        case REVISIT_OK: return "ok";
+        case REVISIT_ERR_NULL: return "null pointer";
+        case REVISIT_ERR_SHAPE: return "bad shape";
+        case REVISIT_ERR_UNSUPPORTED: return "unsupported";
+        case REVISIT_ERR_PARAM: return "bad parameter";
+        case REVISIT_ERR_LAUNCH: return "launch error";
+        default: return "unknown status";
+    }
+}
+
+const char* rc_last_error(void) { return g_last_error; }
+
+int retrieve_chunks(const float* bank_c2w, int32_t n_bank, const float* query_c2w, const int32_t* query_chunk,
+                    int32_t n_query, float E, float w_v, float tau_c, float tau_v, int32_t delta,
+                    int32_t first_candidate, int32_t k, int32_t* out_idx, float* out_score, int32_t* out_count,
+                    int32_t frames_per_chunk, int32_t* out_frame_sel, hipStream_t stream) {
+    if (n_bank < 0 || n_query < 0) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: negative n_bank or n_query");
+    if (k < 1 || k > REVISIT_MAX_K) return fail(REVISIT_ERR_PARAM, "retrieve_chunks: k=%d outside [1, %d]", k, REVISIT_MAX_K);
+    if (!(finite(E) && E > 0.0f)) return fail(REVISIT_ERR_PARAM, "retrieve_chunks: E must be finite and > 0");
+    if (!finite(w_v) || !finite(tau_c) || !finite(tau_v))
+        return fail(REVISIT_ERR_PARAM, "retrieve_chunks: w_v, tau_c and tau_v must be finite");
+    if (out_frame_sel && (frames_per_chunk < 1 || (int64_t)k * frames_per_chunk > (1 << 20)))
+        return fail(REVISIT_ERR_PARAM, "retrieve_chunks: frames_per_chunk=%d invalid", frames_per_chunk);
+    if (n_query == 0) return REVISIT_OK;
+    if (!query_c2w || !query_chunk || !out_idx || !out_count || (n_bank > 0 && !bank_c2w))
+        return fail(REVISIT_ERR_NULL, "retrieve_chunks: required pointer is NULL");
+    revisit::RetrieveArgs a;
+    a.bank_c2w = bank_c2w;
+    a.n_bank = n_bank;
+    a.query_c2w = query_c2w;
+    a.query_chunk = query_chunk;
+    a.n_query = n_query;
+    a.E = (double)E;
+    a.w_v = (double)w_v;
+    a.tau_c = (double)tau_c;
+    a.cos_tau_v = cos((double)tau_v);
+    a.delta = delta;
+    a.first_candidate = first_candidate;
+    a.k = k;
+    a.out_idx = out_idx;
+    a.out_score = out_score;
+    a.out_count = out_count;
+    a.frames_per_chunk = frames_per_chunk;
+    a.out_frame_sel = out_frame_sel;
+    return launched(revisit::launch_retrieve(a, stream), "retrieve_chunks");
+}
+
+int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const float* tgt_K,
+                             const float* src_depth, const float* src_c2w, const float* src_K,
+                             const int32_t* src_sel, int32_t n_src, int32_t B, int32_t Tq, int32_t S, int32_t h,
+                             int32_t w, int32_t p, float eps, float* out_uv, int32_t* out_idx, hipStream_t stream) {
+    if (B < 0 || Tq < 0 || S < 0 || h < 1 || w < 1 || p < 1)
+        return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: need B, Tq, S >= 0 and h, w, p >= 1");
+    if ((int64_t)h * w * p * p > ((int64_t)1 << 28) || (int64_t)h * p > (1 << 20) || (int64_t)w * p > (1 << 20))
+        return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: frame too large");
+    if ((int64_t)B * Tq * h * w > ((int64_t)1 << 31) - 1 || (int64_t)B * S * Tq * h * w > kMaxElems)
+        return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: problem too large");
+    if (src_sel && n_src < 0) return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: n_src < 0");
+    if (!(finite(eps) && eps >= 0.0f)) return fail(REVISIT_ERR_PARAM, "reproject_correspondence: eps must be finite and >= 0");
+    if (B == 0 || Tq == 0 || S == 0) return REVISIT_OK;
+    if (!tgt_depth || !tgt_c2w || !tgt_K || !out_uv || !out_idx)
+        return fail(REVISIT_ERR_NULL, "reproject_correspondence: required pointer is NULL");
+    if ((!src_sel || n_src > 0) && (!src_depth || !src_c2w || !src_K))
+        return fail(REVISIT_ERR_NULL, "reproject_correspondence: source pointer is NULL");
+    if (!aligned(out_uv, 8) || !aligned(out_idx, 4) || !aligned(tgt_depth, 4) || !aligned(src_depth, 4) ||
+        !aligned(src_sel, 4))
+        return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: out_uv must be 8-byte aligned, arrays 4-byte");
+    revisit::ReprojectArgs a;
+    a.tgt_depth = tgt_depth;
+    a.tgt_c2w = tgt_c2w;
+    a.tgt_K = tgt_K;
+    a.src_depth = src_depth;
+    a.src_c2w = src_c2w;
+    a.src_K = src_K;
+    a.src_sel = src_sel;
+    a.n_src = src_sel ? n_src : 0;
+    a.B = B;
+    a.Tq = Tq;
+    a.S = S;
+    a.h = h;
+    a.w = w;
+    a.p = p;
+    a.eps = (double)eps;
+    a.out_uv = out_uv;
+    a.out_idx = out_idx;
+    return launched(revisit::launch_reproject(a, stream), "reproject_correspondence");
+}
+
+int biased_chunk_attention(const void* q, const void* k, const void* v, void* o, float* lse, int32_t dtype,
+                           int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
+                           const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx, int32_t S,
+                           float softmax_scale, float lambda, float sigma, hipStream_t stream) {
+    if (dtype != REVISIT_BF16 && dtype != REVISIT_F32)
+        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: dtype %d not supported", dtype);
+    if (dtype == REVISIT_BF16 && D != 128)
+        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: bf16 needs D = 128 (got %d)", D);
+    if (dtype == REVISIT_F32 && D != 64 && D != 128)
+        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: fp32 needs D = 64 or 128 (got %d)", D);
+    if (Lq < 0 || Lk < 1 || H < 1 || h < 1 || w < 1 || S < 0)
+        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: need Lq >= 0, Lk >= 1, H, h, w >= 1, S >= 0");
+    if (H > 65535) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: H > 65535");
+    const int64_t hw = (int64_t)h * w;
+    if (Lk % hw != 0) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: Lk=%d not a multiple of h*w=%lld", Lk, (long long)hw);
+    if (Lk / hw > kMaxFrames) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: more than %d KV frames", kMaxFrames);
+    if ((int64_t)Lk * H * D > kMaxElems || (int64_t)Lq * H * D > kMaxElems || (int64_t)S * Lq > kMaxElems)
+        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: problem too large");
+    if (!(finite(softmax_scale) && softmax_scale > 0.0f))
+        return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: softmax_scale must be finite and > 0");
+    if (!(finite(sigma) && sigma > 0.0f)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: sigma must be finite and > 0");
+    if (!finite(lambda)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: lambda must be finite");
+    const float gamma = lambda / (2.0f * sigma * sigma * softmax_scale);
+    if (!finite(gamma)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: lambda / (2 sigma^2 scale) overflows");
+    if (Lq == 0) return REVISIT_OK;
+    const bool bias = S > 0 && lambda != 0.0f;
+    if (!q || !k || !v || !o) return fail(REVISIT_ERR_NULL, "biased_chunk_attention: q, k, v and o are required");
+    if (bias && (!kv_frame_slot || !corr_uv || !corr_idx))
+        return fail(REVISIT_ERR_NULL, "biased_chunk_attention: slot table and correspondence map are required when S > 0");
+    // the kernels move q/k/v/o rows in 16-byte vectors and u^ pairs in 8-byte ones
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) || !aligned(lse, 4) ||
+        (bias && (!aligned(corr_uv, 8) || !aligned(corr_idx, 4) || !aligned(kv_frame_slot, 4))))
+        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: q, k, v, o must be 16-byte aligned, corr_uv 8-byte");
+    revisit::AttentionArgs a;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.lse = lse;
+    a.Lq = Lq;
+    a.Lk = Lk;
+    a.H = H;
+    a.D = D;
+    a.h = h;
+    a.w = w;
+    a.slot = kv_frame_slot;
+    a.corr_uv = corr_uv;
+    a.corr_idx = corr_idx;
+    a.S = bias ? S : 0;
+    a.softmax_scale = softmax_scale;
+    a.lambda = lambda;
+    a.sigma = sigma;
+    const hipError_t e = dtype == REVISIT_BF16 ? revisit::launch_attention_bf16(a, stream)
+                                               : revisit::launch_attention_f32(a, stream);
+    return launched(e, "biased_chunk_attention");
+}
+
+}  // extern "C"

@@ -1,0 +1,127 @@
+"""The C interface without a GPU: the library loads, exports every function
+include/revisit.h declares, and rejects bad arguments with the documented
+status before touching the device."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "revisit.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2607_21848_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("librevisit.so is not built: run `python -m paper_2607_21848_amd.build`")
+    return _lib.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_three_stages():
+    names = declared_functions()
+    for n in ("retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "rc_status_string",
+              "rc_last_error"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_binding_matches_exports(L):
+    from paper_2607_21848_amd import _lib
+    assert set(_lib.EXPORTED) == set(declared_functions())
+
+
+def test_status_strings(L):
+    from paper_2607_21848_amd import _lib
+    assert _lib.status_string(0) == "ok"
+    assert _lib.status_string(4) == "bad parameter"
+    assert _lib.status_string(99) == "unknown status"
+
+
+NULL = None
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+def _retrieve(L, **kw):
+    a = dict(bank=FAKE, n_bank=10, query=FAKE, qchunk=FAKE, n_query=1, E=1.0, w_v=0.5, tau_c=0.1, tau_v=0.5,
+             delta=3, first=1, k=4, idx=FAKE, score=NULL, count=FAKE, F=0, sel=NULL)
+    a.update(kw)
+    return L.retrieve_chunks(a["bank"], a["n_bank"], a["query"], a["qchunk"], a["n_query"], a["E"], a["w_v"],
+                             a["tau_c"], a["tau_v"], a["delta"], a["first"], a["k"], a["idx"], a["score"],
+                             a["count"], a["F"], a["sel"], NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=0), 4), (dict(k=33), 4), (dict(E=0.0), 4), (dict(E=float("nan")), 4), (dict(tau_c=float("inf")), 4),
+    (dict(n_bank=-1), 2), (dict(n_query=-2), 2), (dict(query=NULL), 1), (dict(count=NULL), 1),
+    (dict(sel=FAKE, F=0), 4),
+])
+def test_retrieve_rejects(L, kw, status):
+    from paper_2607_21848_amd import _lib
+    assert _retrieve(L, **kw) == status
+    assert len(_lib.last_error()) > 0
+
+
+def test_retrieve_empty_query_is_ok(L):
+    assert _retrieve(L, n_query=0, query=NULL, qchunk=NULL, idx=NULL, count=NULL) == 0
+
+
+def _reproject(L, **kw):
+    a = dict(td=FAKE, tc=FAKE, tk=FAKE, sd=FAKE, sc=FAKE, sk=FAKE, sel=NULL, n_src=0, B=1, Tq=3, S=6, h=30, w=52,
+             p=2, eps=0.05, uv=FAKE, idx=FAKE)
+    a.update(kw)
+    return L.reproject_correspondence(a["td"], a["tc"], a["tk"], a["sd"], a["sc"], a["sk"], a["sel"], a["n_src"],
+                                      a["B"], a["Tq"], a["S"], a["h"], a["w"], a["p"], a["eps"], a["uv"], a["idx"],
+                                      NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(h=0), 2), (dict(p=0), 2), (dict(B=-1), 2), (dict(eps=-0.1), 4), (dict(eps=float("nan")), 4),
+    (dict(td=NULL), 1), (dict(uv=NULL), 1), (dict(sd=NULL), 1), (dict(sel=FAKE, n_src=-1), 2),
+    (dict(h=1 << 20, w=1 << 20), 2),
+])
+def test_reproject_rejects(L, kw, status):
+    assert _reproject(L, **kw) == status
+
+
+def test_reproject_empty_is_ok(L):
+    assert _reproject(L, S=0, td=NULL, uv=NULL) == 0
+    assert _reproject(L, B=0, td=NULL, uv=NULL) == 0
+
+
+def _attention(L, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=NULL, dtype=1, Lq=4680, Lk=28080, H=12, D=128, h=30, w=52,
+             slot=FAKE, uv=FAKE, idx=FAKE, S=6, scale=1 / math.sqrt(128), lam=1.0, sigma=2.0)
+    a.update(kw)
+    return L.biased_chunk_attention(a["q"], a["k"], a["v"], a["o"], a["lse"], a["dtype"], a["Lq"], a["Lk"], a["H"],
+                                    a["D"], a["h"], a["w"], a["slot"], a["uv"], a["idx"], a["S"], a["scale"],
+                                    a["lam"], a["sigma"], NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), 3), (dict(D=64), 3), (dict(dtype=2, D=96), 3), (dict(Lk=28081), 2), (dict(Lk=0), 2),
+    (dict(H=0), 2), (dict(Lq=-1), 2), (dict(sigma=0.0), 4), (dict(scale=-1.0), 4), (dict(lam=float("inf")), 4),
+    (dict(sigma=1e-30), 4), (dict(q=NULL), 1), (dict(o=NULL), 1), (dict(uv=NULL), 1), (dict(slot=NULL), 1),
+    (dict(Lk=5000 * 1560), 2),
+])
+def test_attention_rejects(L, kw, status):
+    assert _attention(L, **kw) == status
+
+
+def test_attention_bias_pointers_optional_when_off(L):
+    # S = 0 or lambda = 0 with NULL map pointers passes validation; Lq = 0 then returns before any launch
+    assert _attention(L, Lq=0, S=0, uv=NULL, idx=NULL, slot=NULL) == 0
+    assert _attention(L, Lq=0, lam=0.0, uv=NULL, idx=NULL, slot=NULL) == 0
