@@ -1,0 +1,306 @@
+"""Benchmark of the revisit-consistency hot path on one MI355X.
+
+One step = one query chunk through the whole path, all on the device:
+pose retrieval over the history bank -> reprojection of the chunk's query
+tokens into the retrieved frames -> biased chunk attention, on the
+Wan-1.3B history-bank workload (12 heads, D 128, bf16, Lq 4680, Lk 37440,
+top-4 retrieval from 200 chunks, reprojection into 12 frames). Inputs are
+resident in HBM before the timed region.
+
+Prints one JSON line. ``value`` is the algorithmic attention throughput of
+the whole step (4 Lq Lk D H flops per step / step time). ``roofline``
+describes the dominant kernel (biased attention) from HIP events recorded on
+its launch stream; ``stages`` adds per-stage times, the reprojection
+throughput of a batched launch (1024 independent problems, > 2x the 256 MB
+last-level cache) and retrieval latency; ``cpu_baseline`` times the fp64
+oracle on a bounded sample of the same workload on this host.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "biased-attention TFLOP/s + MFMA util; reprojection tokens/s (Wan-1.3B shape)"
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+BENCH_QUERY = 1  # query chunk n = 225: a full top-4 retrieval
+REPROJ_BATCH = 1024
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def host_info():
+    cpu = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cpu
+
+
+def blas_threads():
+    for var in ("OPENBLAS_NUM_THREADS", "OMP_NUM_THREADS"):
+        if os.environ.get(var):
+            try:
+                return min(int(os.environ[var]), len(os.sched_getaffinity(0)))
+            except ValueError:
+                pass
+    return len(os.sched_getaffinity(0))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run a plain device-to-device copy of this many MiB (5 times), the reference "
+                         "kernel for scaling HBM byte counters")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the path shards "
+              "per head / per query token across GPUs by design, but no multi-GPU run is part of it", flush=True)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_21848_amd as rv
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", flush=True)
+        sys.exit(1)
+    rv.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    def tb(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    log("generating the Wan-1.3B history-bank workload")
+    wl = W.make_c4("bf16")
+    r = wl.retrieval
+    qs = slice(BENCH_QUERY, BENCH_QUERY + 1)
+    # device-resident inputs
+    bank_c2w, bank_fd, bank_fc, bank_fk = t(r.bank_c2w), t(r.bank_frame_depth), t(r.bank_frame_c2w), t(r.bank_frame_K)
+    q_c2w, q_chunk = t(r.query_c2w[qs]), t(r.query_chunk[qs])
+    tgt_d, tgt_c, tgt_k = t(r.query_frame_depth[qs]), t(r.query_frame_c2w[qs]), t(r.query_frame_K[qs])
+    q, k, v = tb(wl.q), tb(wl.k), tb(wl.v)
+    slot = t(wl.slot)
+    # preallocated outputs: the timed loop allocates nothing
+    ridx = torch.empty((1, r.k), dtype=torch.int32, device=dev)
+    rscore = torch.empty((1, r.k), dtype=torch.float32, device=dev)
+    rcount = torch.empty((1,), dtype=torch.int32, device=dev)
+    rsel = torch.empty((1, r.k * 3), dtype=torch.int32, device=dev)
+    cuv = torch.empty((1, wl.S, wl.Lq, 2), dtype=torch.float32, device=dev)
+    cidx = torch.empty((1, wl.S, wl.Lq), dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty((wl.H, wl.Lq), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        rv.retrieve_chunks(bank_c2w, q_c2w, q_chunk, E=r.E, w_v=r.w_v, tau_c=r.tau_c, tau_v=r.tau_v, delta=r.delta,
+                           first_candidate=r.first_candidate, k=r.k, frames_per_chunk=3,
+                           out=(ridx, rscore, rcount, rsel))
+        if ev is not None:
+            ev[1].record(stream)
+        rv.reproject_correspondence(tgt_d, tgt_c, tgt_k, bank_fd, bank_fc, bank_fk, p=wl.p, eps=wl.eps,
+                                    src_sel=rsel, out=(cuv, cidx))
+        if ev is not None:
+            ev[2].record(stream)
+        rv.biased_chunk_attention(q, k, v, slot, cuv[0], cidx[0], h=wl.h, w=wl.w, softmax_scale=wl.softmax_scale,
+                                  lam=wl.lam, sigma=wl.sigma, out=(o, lse))
+        if ev is not None:
+            ev[3].record(stream)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = 1e3 * wall / args.steps
+    st_ms = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])] for e in evs])
+    retr_ms, repr_ms, attn_ms = st_ms.mean(axis=0)
+    flops = wl.flops
+    attn_tflops = flops / (attn_ms * 1e-3) / 1e12
+    value = flops / (ms_step * 1e-3) / 1e12
+    log(f"step {ms_step:.3f} ms; retrieval {retr_ms * 1e3:.1f} us, reprojection {repr_ms * 1e3:.1f} us, "
+        f"attention {attn_ms:.3f} ms = {attn_tflops:.1f} TFLOP/s")
+
+    # sanity: the step produced a full retrieval and finite outputs
+    assert int(rcount.item()) == r.k and torch.isfinite(o.float()).all()
+
+    # reprojection throughput: one launch over REPROJ_BATCH independent C3-shaped problems
+    log(f"batched reprojection: {REPROJ_BATCH} problems")
+    arrs = W.make_reproj_batch(REPROJ_BATCH)
+    bt = [t(a) for a in arrs]
+    B, Tq, Hd, Wd = arrs[0].shape
+    S = arrs[3].shape[1]
+    p = 2
+    Lq_r = Tq * (Hd // p) * (Wd // p)
+    buv = torch.empty((B, S, Lq_r, 2), dtype=torch.float32, device=dev)
+    bidx = torch.empty((B, S, Lq_r), dtype=torch.int32, device=dev)
+    for _ in range(3):
+        rv.reproject_correspondence(*bt, p=p, eps=0.05, out=(buv, bidx))
+    reps = 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        rv.reproject_correspondence(*bt, p=p, eps=0.05, out=(buv, bidx))
+    e1.record(stream)
+    torch.cuda.synchronize()
+    rb_ms = e0.elapsed_time(e1) / reps
+    tokens = B * Lq_r
+    # algorithmic bytes per query token: p^2 depth pixels in, S (u^ pair + code) out, and the
+    # problem's S source depth maps shared by its Lq_r tokens
+    bytes_per_token = p * p * 4 + S * 12 + S * Hd * Wd * 4 / Lq_r
+    rb_gbs = tokens * bytes_per_token / (rb_ms * 1e-3) / 1e9
+    log(f"batched reprojection {rb_ms:.3f} ms: {tokens / (rb_ms * 1e-3):.3e} tokens/s, {rb_gbs:.0f} GB/s algorithmic")
+    del bt, buv, bidx
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "wan1.3b-history-bank: top-4 retrieval over 200 chunks -> reprojection into 12 frames "
+                        "-> biased attention H12 D128 Lq4680 Lk37440 bf16",
+            "heads": wl.H, "head_dim": wl.D, "Lq": wl.Lq, "Lk": wl.Lk, "token_grid": [wl.h, wl.w],
+            "retrieved_frames": wl.S, "bank_chunks": int(r.bank_c2w.shape[0]), "top_k": r.k,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "attn_bf16_kernel",
+            "achieved": round(attn_tflops, 2),
+            "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+            "flops_per_launch": flops,
+            "avg_launch_ms": round(attn_ms, 4),
+        },
+        "stages": {
+            "retrieval_us": round(retr_ms * 1e3, 2),
+            "reprojection_us": round(repr_ms * 1e3, 2),
+            "reprojection_tokens_per_s_single_chunk": round(wl.Lq / (repr_ms * 1e-3), 0),
+            "attention_ms": round(attn_ms, 4),
+            "attention_tflops": round(attn_tflops, 2),
+            "reprojection_batched": {
+                "problems": B, "tokens": tokens, "ms": round(rb_ms, 4),
+                "tokens_per_s": round(tokens / (rb_ms * 1e-3), 0),
+                "bytes_per_token": bytes_per_token,
+                "achieved_GBs": round(rb_gbs, 1), "peak_GBs": HBM_PEAK_GBS,
+                "frac": round(rb_gbs / HBM_PEAK_GBS, 4), "bound": "hbm",
+            },
+        },
+    }
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = n * 4
+        del src, dst
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(wl, target_s):
+    """The fp64 oracle on this host: retrieval + reprojection of the same
+    query chunk, then attention for blocks of 64 query rows (all heads,
+    all Lk keys) until about ``target_s`` seconds have passed. Reported in the
+    metric's unit: attention flops processed per second."""
+    from oracle import attention as OA, reprojection as OR, retrieval as ORT
+
+    r = wl.retrieval
+    qs = slice(BENCH_QUERY, BENCH_QUERY + 1)
+    log("cpu baseline: oracle retrieval + reprojection")
+    t0 = time.perf_counter()
+    oi, _, oc = ORT.retrieve(r.bank_c2w, r.query_c2w[qs], r.query_chunk[qs], r.E, r.w_v, r.tau_c, r.tau_v, r.delta,
+                             r.first_candidate, r.k)
+    sel = ORT.frame_selection(oi, oc, 3)[0]
+    t1 = time.perf_counter()
+    uv, idx = OR.reproject(r.query_frame_depth[BENCH_QUERY], r.query_frame_c2w[BENCH_QUERY],
+                           r.query_frame_K[BENCH_QUERY], r.bank_frame_depth, r.bank_frame_c2w, r.bank_frame_K,
+                           wl.p, wl.eps, src_sel=sel)
+    t2 = time.perf_counter()
+    qv, kv, vv = wl.values("q"), wl.values("k"), wl.values("v")
+    rows_done = 0
+    block = 64
+    t3 = time.perf_counter()
+    while rows_done < wl.Lq and time.perf_counter() - t3 < target_s:
+        rows = np.arange(rows_done, min(rows_done + block, wl.Lq))
+        OA.biased_attention(qv, kv, vv, wl.slot, uv, idx, wl.h, wl.w, wl.softmax_scale, wl.lam, wl.sigma,
+                            rows=rows, block=block)
+        rows_done += len(rows)
+        log(f"cpu baseline: {rows_done} query rows, {time.perf_counter() - t3:.1f} s")
+    t4 = time.perf_counter()
+    attn_flops = 4.0 * rows_done * wl.Lk * wl.D * wl.H
+    attn_s = t4 - t3
+    # whole-chunk estimate: attention scaled to all Lq rows plus the measured retrieval + reprojection
+    chunk_s = attn_s * wl.Lq / rows_done + (t2 - t0)
+    return {
+        "value": round(attn_flops / attn_s / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": blas_threads(),
+        "kind": "oracle",
+        "sample": f"fp64 NumPy oracle on the bench chunk: retrieval ({1e3 * (t1 - t0):.1f} ms) + reprojection "
+                  f"({1e3 * (t2 - t1):.1f} ms, 1 core) + biased attention for {rows_done} of {wl.Lq} query rows, "
+                  f"all {wl.H} heads and {wl.Lk} keys ({attn_s:.1f} s, BLAS threads); value = attention flops / "
+                  f"attention time; whole chunk extrapolates to {chunk_s:.1f} s",
+        "host_cpu": host_info(),
+        "chunk_seconds_extrapolated": round(chunk_s, 2),
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -173,7 +173,7 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
  *   q           [Lq][H][D], k, v [Lk][H][D], o [Lq][H][D] in dtype
  *               (fp32 accumulation and softmax in both cases)
  *   lse         nullable [H][Lq] fp32
- *   Lq >= 0, Lk >= 1, Lk % (h*w) == 0, Lk / (h*w) <= 4096 KV frames
+ *   Lq >= 0, Lk >= 1, Lk % (h*w) == 0, Lk / (h*w) <= 1024 KV frames
  *   kv_frame_slot [Lk/(h*w)] int32: s in [0, S) for a retrieved frame, any
  *               other value = unbiased (anchor / recent / current frames)
  *   corr_uv     [S][Lq][2] fp32, corr_idx [S][Lq] int32 (reproject_correspondence

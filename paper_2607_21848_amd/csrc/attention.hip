@@ -54,7 +54,7 @@ __device__ __forceinline__ int acc_row(int hh, int i) { return 8 * (i >> 2) + 4 
 struct BiasGeom {
     float gamma;  // lambda / (2 sigma^2 softmax_scale)
     float cx, cy;  // grid centre (w / 2, h / 2)
-    int hw, w;
+    int hw, w, h;
 };
 
 // Frame of `key` and its centred token coordinates.
@@ -207,21 +207,63 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
 
 // ---------------------------------------------------------------------------
 // bf16 kernel: v_mfma_f32_32x32x16_bf16, D = 128. 4 waves x 32 queries per
-// workgroup; 64-key tiles (two 32-row MFMA blocks); K staged row-major and V
-// staged transposed in LDS; the next tile is prefetched into registers while
-// the current one is consumed.
+// workgroup, 64-key tiles (two 32-row MFMA blocks), two workgroups per CU.
+//
+// Memory path. K and V tiles travel global -> LDS with direct 16-byte loads
+// (no register staging, no VALU). Both stay in their natural [key][d]
+// layout (256-byte rows) with the 16-byte chunks of row r stored at chunk
+// position c ^ swz(r). K rows are read with 16-byte LDS loads (the A operand
+// of S^T = K Q^T); V is read with the LDS transpose load (ds_read_b64_tr_b16),
+// which hands each lane 4 keys of one column d, so the A operand of
+// O^T = V^T P^T needs no transposed copy. swz makes both access patterns hit
+// 16 distinct chunk positions per 256 bytes.
+//
+// Pipeline. K runs one tile ahead of V: in step j a wave computes
+// S_{j+1} = K_{j+1} Q^T on the matrix cores while its VALU turns S_j into
+// probabilities, then accumulates O += P_j V_j while the VALU reduces the
+// row maxima of S_{j+1}. Instruction groups are interleaved explicitly
+// (MFMA / LDS / VALU), so the exponentials hide behind the matrix work of
+// the same wave, and the second wave of the SIMD fills remaining gaps. Two
+// K and two V buffers; the loads for tiles j+2 (K) and j+1 (V) are issued
+// right after the one barrier of step j.
+//
+// Softmax. exp2 on the raw hardware instruction with scale * log2(e) folded
+// into one FMA, probabilities packed to bf16 pairwise and summed with bf16
+// dot products (the row sum then matches the rounded P fed to the PV
+// product), and a lazy rescale that only touches O when a row maximum grows
+// by more than 2^8.
+//
+// Bias. The four key/query factor pairs are laid out separably over the
+// two halves of the MFMA contraction: lanes of the first half carry the
+// column terms [2 a_x (x3), -gamma a_x^2 (3 pieces), 1, 1], lanes of the
+// second half the row terms [2 a_y (x3), -gamma a_y^2 (3 pieces), 1, 0]; the
+// query side is [gamma u'_x (3 pieces), 1, 1, 1, q0_hi, q0_mid] and
+// [gamma u'_y (3 pieces), 1, 1, 1, q0_lo, 0] with q0 = -gamma |u'|^2. A key
+// operand is then one 16-byte read from a per-workgroup table indexed by the
+// key's column (first half) or row (second half).
 // ---------------------------------------------------------------------------
 constexpr int kD = 128;
 constexpr int kTK = 64;
-constexpr int kKPitch = kD + 8;    // bf16 elements per K row in LDS (272 B)
-constexpr int kVPitch = kTK + 8;   // bf16 elements per V^T row in LDS (144 B)
-constexpr float kRescaleSlack = 8.0f;  // lazy rescale: tolerate p up to 2^8
+constexpr int kRowBytes = kD * 2;             // 256
+constexpr int kTileBytes = kTK * kRowBytes;   // 16 KB per K or V tile
+constexpr float kRescaleSlack = 8.0f;         // lazy rescale: tolerate p up to 2^8
+constexpr int kMaxFramesLds = 1024;           // KV frames (slot table entries) of the bf16 kernel
+constexpr int kMaxGridSide = 256;             // token-grid rows / columns of the bf16 bias tables
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // Row swap that makes a half-wave's accumulator registers 8t..8t+7 hold 8
 // consecutive keys: exchanges bits 2 and 3 of the row index.
 __device__ __forceinline__ int perm_row(int m) { return (m & ~12) | ((m & 8) >> 1) | ((m & 4) << 1); }
+
+// Chunk swizzle of LDS row r (16 chunks of 16 bytes per row).
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 
 __device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
     const __bf16 b = (__bf16)x;
@@ -240,9 +282,87 @@ __device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uin
 
 __device__ __forceinline__ uint32_t pack2(uint32_t lo16, uint32_t hi16) { return lo16 | (hi16 << 16); }
 
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, BiasGeom g, float c_log2, bool bias_on) {
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kTK * kKPitch];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[kD * kVPitch];
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2){lo, hi}, bf16x2));
+}
+
+// max(a, b, c) in one instruction (the logits are finite or -inf, never NaN)
+__device__ __forceinline__ float max3(float a, float b, float c) {
+    float r;
+    asm volatile("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
+// max / sum of x over the lane and its partner in the other wave half
+__device__ __forceinline__ float half_swap_max(float x) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float half_swap_sum(float x) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
+// Direct global -> LDS loads of one K or V tile. Wave `wave` fills LDS bytes
+// [wave * 4 KB, wave * 4 KB + 4 KB) of the tile with four 1 KB instructions
+// (64 lanes x 16 bytes). Lane byte offsets relative to the tile's first row
+// are fixed for the whole kernel (`off`); only the uniform base moves. On the
+// last tile, rows past Lk are redirected to the last valid row (their logits
+// are masked), so no load leaves the tensor.
+struct TileLoad {
+    uint32_t off[4];  // byte offset of this lane's chunk from the tile's first row
+};
+
+__device__ __forceinline__ void tile_chunk(int wave, int lane, int i, int& r, int& lc) {
+    const int pos = (wave * 4 + i) * 64 + lane;  // 16-byte chunk position in the tile
+    r = pos >> 4;
+    lc = (pos & 15) ^ swz(r);                    // logical chunk stored at this position
+}
+
+__device__ __forceinline__ TileLoad make_tile_load(size_t row_stride, int hd, int wave, int lane) {
+    TileLoad t;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        int r, lc;
+        tile_chunk(wave, lane, i, r, lc);
+        t.off[i] = (uint32_t)(r * (int)(row_stride * 2) + (hd * kD + lc * 8) * 2);
+    }
+    return t;
+}
+
+__device__ __forceinline__ void load_tile_lds(const uint16_t* __restrict__ src, uint8_t* lds_tile, int tile0,
+                                              int Lk, size_t row_stride, const TileLoad& tl, int hd, int wave,
+                                              int lane) {
+    const uint8_t* base = reinterpret_cast<const uint8_t*>(src) + (size_t)tile0 * row_stride * 2;
+    if (tile0 + kTK <= Lk) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            __builtin_amdgcn_global_load_lds(base + tl.off[i], (lds_void*)(lds_tile + (wave * 4 + i) * 1024), 16, 0, 0);
+        }
+    } else {
+        const int last = Lk - 1 - tile0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            int r, lc;
+            tile_chunk(wave, lane, i, r, lc);
+            const uint32_t off = (uint32_t)(min(r, last) * (int)(row_stride * 2) + (hd * kD + lc * 8) * 2);
+            __builtin_amdgcn_global_load_lds(base + off, (lds_void*)(lds_tile + (wave * 4 + i) * 1024), 16, 0, 0);
+        }
+    }
+}
+
+// Scheduling-group masks of the interleave hints.
+constexpr int kSchedMfma = 0x008, kSchedValu = 0x002, kSchedDsRead = 0x100;
+
+template <bool kBias>
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, BiasGeom g, float c_log2) {
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[kTileBytes];
+    __shared__ int lds_slot[kBias ? kMaxFramesLds : 1];        // KV frame -> retrieved frame (or -1)
+    __shared__ u32x4 lds_col[kBias ? kMaxGridSide : 1];        // key operand, first contraction half, by column
+    __shared__ u32x4 lds_row[kBias ? kMaxGridSide : 1];        // key operand, second contraction half, by row
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -258,6 +378,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     const uint16_t* Kg = static_cast<const uint16_t*>(a.k);
     const uint16_t* Vg = static_cast<const uint16_t*>(a.v);
     const size_t row_stride = (size_t)H * kD;  // elements between consecutive tokens
+    const int n_tiles = (Lk + kTK - 1) / kTK;
+
+    // start streaming the first tiles before anything else
+    const TileLoad tl = make_tile_load(row_stride, hd, wave, lane);
+    load_tile_lds(Kg, lds_k0, 0, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Vg, lds_v0, 0, Lk, row_stride, tl, hd, wave, lane);
+    if (n_tiles > 1) load_tile_lds(Kg, lds_k1, kTK, Lk, row_stride, tl, hd, wave, lane);
 
     // Q fragments: lane (hh, n) holds Q[q][16 kk + 8 hh .. +8)
     bf16x8 qf[8];
@@ -268,147 +395,218 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         qf[kk] = as_bf16x8(v);
     }
 
-    // staging assignment: K chunk c = tid + 256 r -> row c / 16, col (c % 16) * 8;
-    // V: key pair pi = tid % 32 (keys 2pi, 2pi+1), d-chunks dc and dc + 8
-    const int v_pi = tid & 31;
-    const int v_dc = tid >> 5;
-    u32x4 kreg[4], vreg[4];
-    auto load_tile = [&](int tile0) {
+    // LDS byte offsets (within a tile) of this lane's operand reads
+    const int krow = perm_row(n);
+    int koff[8];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int c = tid + 256 * r;
-            const int row = c >> 4;
-            const int col = (c & 15) * 8;
-            const int key = tile0 + row;
-            kreg[r] = key < Lk ? *reinterpret_cast<const u32x4*>(Kg + (size_t)key * row_stride + (size_t)hd * kD + col)
-                               : u32x4{0, 0, 0, 0};
+    for (int kk = 0; kk < 8; ++kk) koff[kk] = krow * kRowBytes + (((2 * kk + hh) ^ swz(krow)) << 4);
+    // V transpose reads: lane t of 16-lane group G reads row 8 hh + t / 4 (+4 for the
+    // second half) at columns 32 db + 16 (G % 2) + 4 (t % 4) .. +3
+    const int t16 = lane & 15;
+    const int grp = lane >> 4;
+    const int vrow0 = 8 * hh + (t16 >> 2);
+    const int vcc = 2 * (grp & 1) + ((t16 >> 1) & 1);
+    const int vbyte = 8 * (t16 & 1);
+    int voff[2][4];
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+            const int r = vrow0 + 4 * half;
+            voff[half][db] = r * kRowBytes + (((4 * db + vcc) ^ swz(r)) << 4) + vbyte;
         }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int key = tile0 + 2 * v_pi + (r & 1);
-            const int col = (v_dc + 8 * (r >> 1)) * 8;
-            vreg[r] = key < Lk ? *reinterpret_cast<const u32x4*>(Vg + (size_t)key * row_stride + (size_t)hd * kD + col)
-                               : u32x4{0, 0, 0, 0};
+    }
+
+    // ---- bias state -------------------------------------------------------
+    const int n_frames = Lk / g.hw;
+    const uint32_t one_bf = 0x3f80u;
+    if (kBias) {
+        for (int f = tid; f < n_frames; f += 256) {
+            const int sv = a.slot[f];
+            lds_slot[f] = (sv >= 0 && sv < a.S) ? sv : -1;
         }
-    };
-    auto store_tile = [&]() {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int c = tid + 256 * r;
-            *reinterpret_cast<u32x4*>(Ks + (c >> 4) * kKPitch + (c & 15) * 8) = kreg[r];
+        for (int i = tid; i < g.w + g.h; i += 256) {
+            const bool col = i < g.w;
+            const int k = col ? i : i - g.w;
+            const float ac = ((float)k + 0.5f) - (col ? g.cx : g.cy);
+            const uint32_t a2 = bf16_bits_rne(2.0f * ac);
+            uint32_t ph, pm, pl;
+            split3(-g.gamma * (ac * ac), ph, pm, pl);
+            const u32x4 v = u32x4{pack2(a2, a2), pack2(a2, ph), pack2(pm, pl), col ? pack2(one_bf, one_bf) : one_bf};
+            if (col) lds_col[k] = v;
+            else lds_row[k] = v;
         }
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            const u32x4 k0 = vreg[2 * half], k1 = vreg[2 * half + 1];
-            const int d0 = (v_dc + 8 * half) * 8;
-#pragma unroll
-            for (int wd = 0; wd < 4; ++wd) {
-                // elements 2wd (low halves) and 2wd+1 (high halves) of both keys
-                const uint32_t lo = (k0[wd] & 0xffffu) | (k1[wd] << 16);
-                const uint32_t hi = (k0[wd] >> 16) | (k1[wd] & 0xffff0000u);
-                *reinterpret_cast<uint32_t*>(Vt + (d0 + 2 * wd) * kVPitch + 2 * v_pi) = lo;
-                *reinterpret_cast<uint32_t*>(Vt + (d0 + 2 * wd + 1) * kVPitch + 2 * v_pi) = hi;
+    }
+    // query-side operands of the frames the next QK tile can touch, by frame
+    int qb_frame[2] = {-1, -1};
+    bf16x8 qb[2] = {as_bf16x8(u32x4{0, 0, 0, 0}), as_bf16x8(u32x4{0, 0, 0, 0})};
+    auto query_operand = [&](int s) -> bf16x8 {
+        u32x4 v = u32x4{0, 0, 0, 0};
+        if (s >= 0 && q_ok) {
+            const size_t o = (size_t)s * a.Lq + q;
+            if (a.corr_idx[o] >= 0) {
+                const float2 u = reinterpret_cast<const float2*>(a.corr_uv)[o];
+                const float ux = u.x - g.cx, uy = u.y - g.cy;
+                uint32_t xh, xm, xl, yh, ym, yl, zh, zm, zl;
+                split3(g.gamma * ux, xh, xm, xl);
+                split3(g.gamma * uy, yh, ym, yl);
+                split3(-g.gamma * (ux * ux + uy * uy), zh, zm, zl);
+                if (hh == 0) v = u32x4{pack2(xh, xm), pack2(xl, one_bf), pack2(one_bf, one_bf), pack2(zh, zm)};
+                else v = u32x4{pack2(yh, ym), pack2(yl, one_bf), pack2(one_bf, one_bf), zl};
             }
         }
+        return as_bf16x8(v);
     };
+    // frame / in-frame offset of the next QK block start (uniform) and of this
+    // lane's key-operand row, both advanced 32 keys per block
+    int blk_f = 0, blk_t = 0;
+    int lane_t = krow, lane_f = 0;
+    if (kBias) {
+        while (lane_t >= g.hw) {
+            lane_t -= g.hw;
+            ++lane_f;
+        }
+    }
+    const float inv_w = 1.0f / (float)g.w;
 
-    floatx16 O[4];
-#pragma unroll
-    for (int db = 0; db < 4; ++db) O[db] = floatx16{0};
-    float m_run = -INFINITY, l_run = 0.0f;
-    const int n_frames = Lk / g.hw;
-
-    // query-side bias operand, rebuilt when the retrieved frame changes
-    int cached_s = -1;
-    bf16x8 qb = as_bf16x8(u32x4{0, 0, 0, 0});
-
-    const int n_tiles = (Lk + kTK - 1) / kTK;
-    load_tile(0);
-    for (int it = 0; it < n_tiles; ++it) {
-        const int tile0 = it * kTK;
-        __syncthreads();
-        store_tile();
-        __syncthreads();
-        if (it + 1 < n_tiles) load_tile(tile0 + kTK);
-
-        floatx16 acc[2];
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            acc[rb] = floatx16{0};
-            const int k0 = tile0 + 32 * rb;
-            if (bias_on && k0 < Lk) {
-                const int k_last = min(k0 + 31, Lk - 1);
-                const int f0 = k0 / g.hw, f1 = k_last / g.hw;
-                for (int f = f0; f <= f1 && f < n_frames; ++f) {
-                    const int s = a.slot[f];
-                    if (s < 0 || s >= a.S) continue;
-                    if (s != cached_s) {
-                        bool valid;
-                        float gx, gy, q0;
-                        query_factors(a.corr_uv, a.corr_idx, a.Lq, s, q, g, valid, gx, gy, q0);
-                        uint32_t xh, xm, xl, yh, ym, yl, zh, zm, zl;
-                        split3(gx, xh, xm, xl);
-                        split3(gy, yh, ym, yl);
-                        split3(q0, zh, zm, zl);
-                        const uint32_t one = 0x3f80u;
-                        u32x4 v;
-                        if (hh == 0) v = u32x4{pack2(xh, xm), pack2(xl, yh), pack2(ym, yl), pack2(one, one)};
-                        else v = u32x4{pack2(one, zh), pack2(zm, zl), 0u, 0u};
-                        if (!valid) v = u32x4{0, 0, 0, 0};
-                        qb = as_bf16x8(v);
-                        cached_s = s;
-                    }
-                    int kf;
-                    float ax, ay;
-                    const int key = k0 + perm_row(n);
-                    key_coords(key, g, kf, ax, ay);
-                    const bool in_f = key <= k_last && kf == f;
-                    u32x4 kv = u32x4{0, 0, 0, 0};
-                    if (in_f) {
-                        const uint32_t x2 = bf16_bits_rne(2.0f * ax), y2 = bf16_bits_rne(2.0f * ay);
-                        uint32_t kh, km, kl;
-                        split3(-g.gamma * (ax * ax + ay * ay), kh, km, kl);
-                        const uint32_t one = 0x3f80u;
-                        if (hh == 0) kv = u32x4{pack2(x2, x2), pack2(x2, y2), pack2(y2, y2), pack2(kh, km)};
-                        else kv = u32x4{pack2(kl, one), pack2(one, one), 0u, 0u};
-                    }
-                    acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qb, acc[rb], 0, 0, 0);
+    // Bias prelude of a QK block: returns the accumulator start value (the
+    // bias of a second frame when the block straddles two) and sets the key
+    // and query operands of the main bias MFMA.
+    auto bias_prelude = [&](int k0, bf16x8& kv_out, bf16x8& qv_out) -> floatx16 {
+        floatx16 init = floatx16{0};
+        u32x4 kvA = u32x4{0, 0, 0, 0};
+        bf16x8 qA = as_bf16x8(u32x4{0, 0, 0, 0});
+        const int span = min(31, Lk - 1 - k0);
+        // key operand of this lane's row (masked per frame below)
+        u32x4 krow_op = u32x4{0, 0, 0, 0};
+        const bool row_live = krow <= span;
+        if (row_live) {
+            const int ky = (int)(((float)lane_t + 0.5f) * inv_w);
+            const int kx = lane_t - ky * g.w;
+            krow_op = hh == 0 ? lds_col[kx] : lds_row[ky];
+        }
+        for (int i = 0, f = blk_f, fs = -blk_t; fs <= span && f < n_frames; ++i, ++f, fs += g.hw) {
+            const int s = __builtin_amdgcn_readfirstlane(lds_slot[f]);
+            if (s < 0) continue;
+            int slot_i;
+            if (f == qb_frame[0]) {
+                slot_i = 0;
+            } else if (f == qb_frame[1]) {
+                slot_i = 1;
+            } else {
+                // a frame not seen before: it replaces the older entry
+                slot_i = (qb_frame[0] < qb_frame[1]) ? 0 : 1;
+                const bf16x8 nq = query_operand(s);
+                if (slot_i == 0) {
+                    qb[0] = nq;
+                    qb_frame[0] = f;
+                } else {
+                    qb[1] = nq;
+                    qb_frame[1] = f;
                 }
             }
-            const uint16_t* krow = Ks + (32 * rb + perm_row(n)) * kKPitch + 8 * hh;
-#pragma unroll
-            for (int kk = 0; kk < 8; ++kk) {
-                const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(krow + 16 * kk));
-                acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], acc[rb], 0, 0, 0);
+            const bf16x8 qv = slot_i == 0 ? qb[0] : qb[1];
+            const u32x4 kv = (row_live && lane_f == f) ? krow_op : u32x4{0, 0, 0, 0};
+            if (i == 0) {
+                kvA = kv;
+                qA = qv;
+            } else {
+                init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qv, init, 0, 0, 0);
             }
         }
+        kv_out = as_bf16x8(kvA);
+        qv_out = qA;
+        return init;
+    };
+    auto advance_block = [&]() {
+        blk_t += 32;
+        while (blk_t >= g.hw) {
+            blk_t -= g.hw;
+            ++blk_f;
+        }
+        lane_t += 32;
+        while (lane_t >= g.hw) {
+            lane_t -= g.hw;
+            ++lane_f;
+        }
+    };
 
-        // online softmax; register i of block rb holds key
-        // tile0 + 32 rb + 16 (i / 8) + 8 hh + (i % 8)
-        float mx = -INFINITY;
+    // QK^T of one 64-key tile (two 32-key blocks) from LDS into S
+    auto qk_tile = [&](const uint8_t* kt, int tile0, floatx16 (&S)[2]) {
+        bf16x8 kvb[2], qvb[2];
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+            if (kBias) {
+                S[rb] = bias_prelude(tile0 + 32 * rb, kvb[rb], qvb[rb]);
+                advance_block();
+            } else {
+                S[rb] = floatx16{0};
+            }
+        }
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+            if (kBias) S[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kvb[rb], qvb[rb], S[rb], 0, 0, 0);
+#pragma unroll
+            for (int kk = 0; kk < 8; ++kk) {
+                const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(kt + rb * 32 * kRowBytes + koff[kk]));
+                S[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], S[rb], 0, 0, 0);
+            }
+        }
+    };
+    // mask keys past Lk (last tile only) and reduce this lane's maximum
+    auto tile_max = [&](floatx16 (&S)[2], int tile0) -> float {
         if (tile0 + kTK > Lk) {
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    if (tile0 + 32 * rb + 16 * (i >> 3) + 8 * hh + (i & 7) >= Lk) acc[rb][i] = -INFINITY;
+                    if (tile0 + 32 * rb + 16 * (i >> 3) + 8 * hh + (i & 7) >= Lk) S[rb][i] = -INFINITY;
                 }
             }
         }
+        float m0 = fmaxf(S[0][0], S[0][1]), m1 = fmaxf(S[1][0], S[1][1]);
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[rb][i]);
+        for (int i = 2; i < 16; i += 2) {
+            m0 = max3(m0, S[0][i], S[0][i + 1]);
+            m1 = max3(m1, S[1][i], S[1][i + 1]);
         }
-        mx = fmaxf(mx, __shfl_xor(mx, 32)) * c_log2;
+        return fmaxf(m0, m1);
+    };
+
+    floatx16 O[4];
+#pragma unroll
+    for (int db = 0; db < 4; ++db) O[db] = floatx16{0};
+    float m_run = -INFINITY, l_run0 = 0.0f, l_run1 = 0.0f;
+    const uint32_t ones2 = 0x3f803f80u;  // bf16 (1, 1)
+
+    floatx16 Sa[2], Sb[2];
+    float mx_cur;
+
+    // One pipeline step: softmax + PV of tile j (in S_cur, V in vcur), QK of
+    // tile j + 1 (K in knext) into S_next; loads of K_{j+2} -> kdst and
+    // V_{j+1} -> vdst are issued after the barrier.
+    auto step = [&](int j, floatx16 (&S_cur)[2], floatx16 (&S_next)[2], const uint8_t* vcur, const uint8_t* knext,
+                    uint8_t* kdst, uint8_t* vdst) {
+        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's loads of V_j and K_{j+1} have landed
+        __syncthreads();
+        if (j + 2 < n_tiles) load_tile_lds(Kg, kdst, (j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
+        if (j + 1 < n_tiles) load_tile_lds(Vg, vdst, (j + 1) * kTK, Lk, row_stride, tl, hd, wave, lane);
+
+        // row maximum of tile j (reduced during the previous step) and lazy rescale
+        const float mx = half_swap_max(mx_cur) * c_log2;
         if (__any(mx > m_run + kRescaleSlack)) {
             const float m_new = fmaxf(m_run, mx);
-            const float alpha = exp2f(m_run - m_new);
-            l_run *= alpha;
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            l_run0 *= alpha;
+            l_run1 *= alpha;
 #pragma unroll
             for (int db = 0; db < 4; ++db) O[db] *= alpha;
             m_run = m_new;
         }
+        const bool has_next = j + 1 < n_tiles;
+
+        // region A: QK of tile j + 1 on the matrix cores, probabilities of tile j on the VALU
+        if (has_next) qk_tile(knext, (j + 1) * kTK, S_next);
         bf16x8 pf[2][2];
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) {
@@ -417,31 +615,73 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
                 uint32_t w4[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float p0 = exp2f(fmaf(acc[rb][8 * t + 2 * e], c_log2, -m_run));
-                    const float p1 = exp2f(fmaf(acc[rb][8 * t + 2 * e + 1], c_log2, -m_run));
-                    l_run += p0 + p1;
-                    w4[e] = pack2(bf16_bits_rne(p0), bf16_bits_rne(p1));
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(S_cur[rb][8 * t + 2 * e], c_log2, -m_run));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(S_cur[rb][8 * t + 2 * e + 1], c_log2, -m_run));
+                    w4[e] = cvt_pk_bf16(p0, p1);
+                    if (e & 1) {
+                        l_run1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
+                                                                 __builtin_bit_cast(bf16x2, ones2), l_run1, false);
+                    } else {
+                        l_run0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
+                                                                 __builtin_bit_cast(bf16x2, ones2), l_run0, false);
+                    }
                 }
                 pf[rb][t] = as_bf16x8(u32x4{w4[0], w4[1], w4[2], w4[3]});
             }
         }
+        if (has_next) {
+#pragma unroll
+            for (int i = 0; i < 18; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedValu, 6, 0);
+            }
+        }
 
-        // O^T += V^T P^T
+        // region B: PV of tile j on the matrix cores, row maxima of tile j + 1 on the VALU
+        float mx_next = -INFINITY;
+        if (has_next) mx_next = tile_max(S_next, (j + 1) * kTK);
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
-            const uint16_t* vrow = Vt + (32 * db + n) * kVPitch + 8 * hh;
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {
-                    const bf16x8 vf = as_bf16x8(*reinterpret_cast<const u32x4*>(vrow + 32 * rb + 16 * t));
-                    O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[rb][t], O[db], 0, 0, 0);
+                    const uint8_t* vt = vcur + (32 * rb + 16 * t) * kRowBytes;
+                    const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[0][db]));
+                    const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[1][db]));
+                    u32x4 w;
+                    w[0] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[0], lo[1]});
+                    w[1] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[2], lo[3]});
+                    w[2] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[0], hi[1]});
+                    w[3] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[2], hi[3]});
+                    O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[rb][t], O[db], 0, 0, 0);
                 }
             }
         }
-    }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 1);
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 1);
+            __builtin_amdgcn_sched_group_barrier(kSchedValu, 2, 1);
+        }
+        mx_cur = mx_next;
+    };
 
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    // prologue: S_0
+    __builtin_amdgcn_s_waitcnt(0x0f70);
+    __syncthreads();
+    qk_tile(lds_k0, 0, Sa);
+    mx_cur = tile_max(Sa, 0);
+
+    int j = 0;
+    for (; j + 1 < n_tiles; j += 2) {
+        step(j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+        step(j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
+    }
+    if (j < n_tiles) step(j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+
+    const float l_tot = half_swap_sum(l_run0 + l_run1);
     const float inv = 1.0f / l_tot;
     if (q_ok) {
         uint16_t* Og = static_cast<uint16_t*>(a.o) + (size_t)q * row_stride + (size_t)hd * kD;
@@ -450,8 +690,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
 #pragma unroll
             for (int gi = 0; gi < 4; ++gi) {
                 const int d = 32 * db + 8 * gi + 4 * hh;
-                const uint32_t w0 = pack2(bf16_bits_rne(O[db][4 * gi] * inv), bf16_bits_rne(O[db][4 * gi + 1] * inv));
-                const uint32_t w1 = pack2(bf16_bits_rne(O[db][4 * gi + 2] * inv), bf16_bits_rne(O[db][4 * gi + 3] * inv));
+                const uint32_t w0 = cvt_pk_bf16(O[db][4 * gi] * inv, O[db][4 * gi + 1] * inv);
+                const uint32_t w1 = cvt_pk_bf16(O[db][4 * gi + 2] * inv, O[db][4 * gi + 3] * inv);
                 *reinterpret_cast<uint2*>(Og + d) = make_uint2(w0, w1);
             }
         }
@@ -466,6 +706,7 @@ BiasGeom make_geom(const AttentionArgs& a) {
     g.cy = 0.5f * (float)a.h;
     g.hw = a.h * a.w;
     g.w = a.w;
+    g.h = a.h;
     return g;
 }
 
@@ -490,7 +731,11 @@ hipError_t launch_attention_bf16(const AttentionArgs& a, hipStream_t stream) {
     const BiasGeom g = make_geom(a);
     const bool bias_on = a.S > 0 && a.lambda != 0.0f;
     const dim3 grid((a.Lq + 127) / 128, a.H), block(256);
-    hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e, bias_on);
+    if (bias_on) {
+        hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e);
+    } else {
+        hipLaunchKernelGGL(attn_bf16_kernel<false>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e);
+    }
     return hipGetLastError();
 }
 

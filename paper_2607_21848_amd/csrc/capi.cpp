@@ -34,7 +34,7 @@ bool finite(float x) { return isfinite(x); }
 bool aligned(const void* ptr, uintptr_t bytes) { return ((uintptr_t)ptr % bytes) == 0; }
 
 constexpr int64_t kMaxElems = (int64_t)1 << 40;
-constexpr int kMaxFrames = 4096;
+constexpr int kMaxFrames = 1024;
 
 }  // namespace
 

@@ -115,7 +115,7 @@ def _attention(L, **kw):
     (dict(dtype=7), 3), (dict(D=64), 3), (dict(dtype=2, D=96), 3), (dict(Lk=28081), 2), (dict(Lk=0), 2),
     (dict(H=0), 2), (dict(Lq=-1), 2), (dict(sigma=0.0), 4), (dict(scale=-1.0), 4), (dict(lam=float("inf")), 4),
     (dict(sigma=1e-30), 4), (dict(q=NULL), 1), (dict(o=NULL), 1), (dict(uv=NULL), 1), (dict(slot=NULL), 1),
-    (dict(Lk=5000 * 1560), 2),
+    (dict(Lk=1025 * 1560), 2),
 ])
 def test_attention_rejects(L, kw, status):
     assert _attention(L, **kw) == status
