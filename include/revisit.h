@@ -139,7 +139,8 @@ int retrieve_chunks(const float* bank_c2w, int32_t n_bank,
  *                      and src_sel [B][S] int32 choosing the frame of each slot;
  *                      an entry outside [0, n_src) means "no source" and the
  *                      whole slot is written as REVISIT_NO_SOURCE.
- *   p >= 1 latent pixels per token side; eps >= 0 finite.
+ *   S <= 64 source frames per problem; p >= 1 latent pixels per token side;
+ *   eps >= 0 finite.
  *   out_uv  [B][S][Tq*h*w][2] fp32: u^ in token units (row-major token order,
  *           target frames outer); NaN for UNDEFINED, BEHIND and NO_SOURCE.
  *   out_idx [B][S][Tq*h*w] int32: key index floor(u^_y) w + floor(u^_x) within

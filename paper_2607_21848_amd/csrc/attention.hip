@@ -36,6 +36,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace revisit {
@@ -243,9 +245,9 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
 // key's column (first half) or row (second half).
 // ---------------------------------------------------------------------------
 constexpr int kD = 128;
-constexpr int kTK = 64;
+constexpr int kTK = 32;
 constexpr int kRowBytes = kD * 2;             // 256
-constexpr int kTileBytes = kTK * kRowBytes;   // 16 KB per K or V tile
+constexpr int kTileBytes = kTK * kRowBytes;   // 8 KB per K or V tile
 constexpr float kRescaleSlack = 8.0f;         // lazy rescale: tolerate p up to 2^8
 constexpr int kMaxFramesLds = 1024;           // KV frames (slot table entries) of the bf16 kernel
 constexpr int kMaxGridSide = 256;             // token-grid rows / columns of the bf16 bias tables
@@ -303,18 +305,19 @@ __device__ __forceinline__ float half_swap_sum(float x) {
     return __uint_as_float(p[0]) + __uint_as_float(p[1]);
 }
 
-// Direct global -> LDS loads of one K or V tile. Wave `wave` fills LDS bytes
-// [wave * 4 KB, wave * 4 KB + 4 KB) of the tile with four 1 KB instructions
-// (64 lanes x 16 bytes). Lane byte offsets relative to the tile's first row
+// Direct global -> LDS loads of one K or V tile. Wave `wave` fills its
+// quarter of the tile with 1 KB instructions (64 lanes x 16 bytes). Lane byte offsets relative to the tile's first row
 // are fixed for the whole kernel (`off`); only the uniform base moves. On the
 // last tile, rows past Lk are redirected to the last valid row (their logits
 // are masked), so no load leaves the tensor.
+constexpr int kLoadsPerLane = kTileBytes / (256 * 16);  // 16-byte direct loads per lane per tile
+
 struct TileLoad {
-    uint32_t off[4];  // byte offset of this lane's chunk from the tile's first row
+    uint32_t off[kLoadsPerLane];  // byte offset of this lane's chunk from the tile's first row
 };
 
 __device__ __forceinline__ void tile_chunk(int wave, int lane, int i, int& r, int& lc) {
-    const int pos = (wave * 4 + i) * 64 + lane;  // 16-byte chunk position in the tile
+    const int pos = (wave * kLoadsPerLane + i) * 64 + lane;  // 16-byte chunk position in the tile
     r = pos >> 4;
     lc = (pos & 15) ^ swz(r);                    // logical chunk stored at this position
 }
@@ -322,7 +325,7 @@ __device__ __forceinline__ void tile_chunk(int wave, int lane, int i, int& r, in
 __device__ __forceinline__ TileLoad make_tile_load(size_t row_stride, int hd, int wave, int lane) {
     TileLoad t;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kLoadsPerLane; ++i) {
         int r, lc;
         tile_chunk(wave, lane, i, r, lc);
         t.off[i] = (uint32_t)(r * (int)(row_stride * 2) + (hd * kD + lc * 8) * 2);
@@ -336,17 +339,19 @@ __device__ __forceinline__ void load_tile_lds(const uint16_t* __restrict__ src, 
     const uint8_t* base = reinterpret_cast<const uint8_t*>(src) + (size_t)tile0 * row_stride * 2;
     if (tile0 + kTK <= Lk) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            __builtin_amdgcn_global_load_lds(base + tl.off[i], (lds_void*)(lds_tile + (wave * 4 + i) * 1024), 16, 0, 0);
+        for (int i = 0; i < kLoadsPerLane; ++i) {
+            __builtin_amdgcn_global_load_lds(base + tl.off[i], (lds_void*)(lds_tile + (wave * kLoadsPerLane + i) * 1024),
+                                             16, 0, 0);
         }
     } else {
         const int last = Lk - 1 - tile0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < kLoadsPerLane; ++i) {
             int r, lc;
             tile_chunk(wave, lane, i, r, lc);
             const uint32_t off = (uint32_t)(min(r, last) * (int)(row_stride * 2) + (hd * kD + lc * 8) * 2);
-            __builtin_amdgcn_global_load_lds(base + off, (lds_void*)(lds_tile + (wave * 4 + i) * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(base + off, (lds_void*)(lds_tile + (wave * kLoadsPerLane + i) * 1024), 16,
+                                             0, 0);
         }
     }
 }
@@ -531,46 +536,34 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         }
     };
 
-    // QK^T of one 64-key tile (two 32-key blocks) from LDS into S
-    auto qk_tile = [&](const uint8_t* kt, int tile0, floatx16 (&S)[2]) {
-        bf16x8 kvb[2], qvb[2];
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            if (kBias) {
-                S[rb] = bias_prelude(tile0 + 32 * rb, kvb[rb], qvb[rb]);
-                advance_block();
-            } else {
-                S[rb] = floatx16{0};
-            }
+    // QK^T of one 32-key tile from LDS (buffer kt), bias first, into S
+    auto qk_tile = [&](const uint8_t* kt, int k0, floatx16& S) {
+        bf16x8 kvb, qvb;
+        if constexpr (kBias) {
+            S = bias_prelude(k0, kvb, qvb);
+            advance_block();
+            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kvb, qvb, S, 0, 0, 0);
+        } else {
+            S = floatx16{0};
         }
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            if (kBias) S[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kvb[rb], qvb[rb], S[rb], 0, 0, 0);
-#pragma unroll
-            for (int kk = 0; kk < 8; ++kk) {
-                const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(kt + rb * 32 * kRowBytes + koff[kk]));
-                S[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], S[rb], 0, 0, 0);
-            }
+        for (int kk = 0; kk < 8; ++kk) {
+            const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(kt + koff[kk]));
+            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], S, 0, 0, 0);
         }
     };
-    // mask keys past Lk (last tile only) and reduce this lane's maximum
-    auto tile_max = [&](floatx16 (&S)[2], int tile0) -> float {
-        if (tile0 + kTK > Lk) {
+    // mask keys past Lk (only the last tile can hold any) and reduce this lane's maximum
+    auto tile_max = [&](auto mask_tag, floatx16& S, int k0) -> float {
+        if constexpr (decltype(mask_tag)::value) {
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    if (tile0 + 32 * rb + 16 * (i >> 3) + 8 * hh + (i & 7) >= Lk) S[rb][i] = -INFINITY;
-                }
+            for (int i = 0; i < 16; ++i) {
+                if (k0 + 16 * (i >> 3) + 8 * hh + (i & 7) >= Lk) S[i] = -INFINITY;
             }
         }
-        float m0 = fmaxf(S[0][0], S[0][1]), m1 = fmaxf(S[1][0], S[1][1]);
+        float m = fmaxf(S[0], S[1]);
 #pragma unroll
-        for (int i = 2; i < 16; i += 2) {
-            m0 = max3(m0, S[0][i], S[0][i + 1]);
-            m1 = max3(m1, S[1][i], S[1][i + 1]);
-        }
-        return fmaxf(m0, m1);
+        for (int i = 2; i < 16; i += 2) m = max3(m, S[i], S[i + 1]);
+        return m;
     };
 
     floatx16 O[4];
@@ -578,15 +571,21 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     for (int db = 0; db < 4; ++db) O[db] = floatx16{0};
     float m_run = -INFINITY, l_run0 = 0.0f, l_run1 = 0.0f;
     const uint32_t ones2 = 0x3f803f80u;  // bf16 (1, 1)
+    using True = std::integral_constant<bool, true>;
+    using False = std::integral_constant<bool, false>;
 
-    floatx16 Sa[2], Sb[2];
+    floatx16 Sa, Sb;
     float mx_cur;
 
-    // One pipeline step: softmax + PV of tile j (in S_cur, V in vcur), QK of
-    // tile j + 1 (K in knext) into S_next; loads of K_{j+2} -> kdst and
-    // V_{j+1} -> vdst are issued after the barrier.
-    auto step = [&](int j, floatx16 (&S_cur)[2], floatx16 (&S_next)[2], const uint8_t* vcur, const uint8_t* knext,
-                    uint8_t* kdst, uint8_t* vdst) {
+    // One pipeline step for tile j: barrier, prefetch of K_{j+2} and V_{j+1},
+    // then softmax + PV of tile j (logits in S_cur, V_j in vcur) while the
+    // logits of tile j + 1 (K_{j+1} in knext) are computed into S_next.
+    // Kinds: 0 = tile j + 1 exists and is not the last, 1 = tile j + 1 is the
+    // last (its keys may run past Lk), 2 = tile j is the last.
+    auto step = [&](auto kind_tag, int j, floatx16& S_cur, floatx16& S_next, const uint8_t* vcur,
+                    const uint8_t* knext, uint8_t* kdst, uint8_t* vdst) {
+        constexpr int kind = decltype(kind_tag)::value;
+        constexpr bool has_next = kind != 2;
         __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's loads of V_j and K_{j+1} have landed
         __syncthreads();
         if (j + 2 < n_tiles) load_tile_lds(Kg, kdst, (j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
@@ -603,83 +602,95 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             for (int db = 0; db < 4; ++db) O[db] *= alpha;
             m_run = m_new;
         }
-        const bool has_next = j + 1 < n_tiles;
 
         // region A: QK of tile j + 1 on the matrix cores, probabilities of tile j on the VALU
-        if (has_next) qk_tile(knext, (j + 1) * kTK, S_next);
-        bf16x8 pf[2][2];
+        const int nk0 = (j + 1) * kTK;
+        if constexpr (has_next) qk_tile(knext, nk0, S_next);
+        bf16x8 pf[2];
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
+        for (int t = 0; t < 2; ++t) {
+            uint32_t w4[4];
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                uint32_t w4[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float p0 = __builtin_amdgcn_exp2f(fmaf(S_cur[rb][8 * t + 2 * e], c_log2, -m_run));
-                    const float p1 = __builtin_amdgcn_exp2f(fmaf(S_cur[rb][8 * t + 2 * e + 1], c_log2, -m_run));
-                    w4[e] = cvt_pk_bf16(p0, p1);
-                    if (e & 1) {
-                        l_run1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
-                                                                 __builtin_bit_cast(bf16x2, ones2), l_run1, false);
-                    } else {
-                        l_run0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
-                                                                 __builtin_bit_cast(bf16x2, ones2), l_run0, false);
-                    }
+            for (int e = 0; e < 4; ++e) {
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(S_cur[8 * t + 2 * e], c_log2, -m_run));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(S_cur[8 * t + 2 * e + 1], c_log2, -m_run));
+                w4[e] = cvt_pk_bf16(p0, p1);
+                if (e & 1) {
+                    l_run1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
+                                                             __builtin_bit_cast(bf16x2, ones2), l_run1, false);
+                } else {
+                    l_run0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
+                                                             __builtin_bit_cast(bf16x2, ones2), l_run0, false);
                 }
-                pf[rb][t] = as_bf16x8(u32x4{w4[0], w4[1], w4[2], w4[3]});
             }
+            pf[t] = as_bf16x8(u32x4{w4[0], w4[1], w4[2], w4[3]});
         }
-        if (has_next) {
+        if constexpr (has_next) {
+            // LDS reads run ahead of the MFMAs that consume them
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
 #pragma unroll
-            for (int i = 0; i < 18; ++i) {
-                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            for (int i = 0; i < (kBias ? 9 : 8); ++i) {
                 __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(kSchedValu, 6, 0);
             }
         }
 
-        // region B: PV of tile j on the matrix cores, row maxima of tile j + 1 on the VALU
+        // region B: PV of tile j on the matrix cores, row maximum of tile j + 1 on the VALU
         float mx_next = -INFINITY;
-        if (has_next) mx_next = tile_max(S_next, (j + 1) * kTK);
+        if constexpr (has_next) mx_next = tile_max(std::integral_constant<bool, kind == 1>{}, S_next, nk0);
 #pragma unroll
-        for (int db = 0; db < 4; ++db) {
+        for (int t = 0; t < 2; ++t) {
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-#pragma unroll
-                for (int t = 0; t < 2; ++t) {
-                    const uint8_t* vt = vcur + (32 * rb + 16 * t) * kRowBytes;
-                    const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[0][db]));
-                    const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[1][db]));
-                    u32x4 w;
-                    w[0] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[0], lo[1]});
-                    w[1] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[2], lo[3]});
-                    w[2] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[0], hi[1]});
-                    w[3] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[2], hi[3]});
-                    O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[rb][t], O[db], 0, 0, 0);
-                }
+            for (int db = 0; db < 4; ++db) {
+                const uint8_t* vt = vcur + 16 * t * kRowBytes;
+                const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[0][db]));
+                const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[1][db]));
+                u32x4 w;
+                w[0] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[0], lo[1]});
+                w[1] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[2], lo[3]});
+                w[2] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[0], hi[1]});
+                w[3] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[2], hi[3]});
+                O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t], O[db], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 1);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 1);
+        for (int i = 0; i < 8; ++i) {
             __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 1);
-            __builtin_amdgcn_sched_group_barrier(kSchedValu, 2, 1);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 1);
+            __builtin_amdgcn_sched_group_barrier(kSchedValu, 1, 1);
         }
         mx_cur = mx_next;
     };
+    using Steady = std::integral_constant<int, 0>;
+    using Penult = std::integral_constant<int, 1>;
+    using LastT = std::integral_constant<int, 2>;
 
-    // prologue: S_0
+    // prologue: logits of tile 0
     __builtin_amdgcn_s_waitcnt(0x0f70);
     __syncthreads();
     qk_tile(lds_k0, 0, Sa);
-    mx_cur = tile_max(Sa, 0);
+    mx_cur = n_tiles == 1 ? tile_max(True{}, Sa, 0) : tile_max(False{}, Sa, 0);
 
+    // steady state over pairs of tiles (even tiles: V in v0, K of the next in k1);
+    // then the last one, two or three tiles
     int j = 0;
-    for (; j + 1 < n_tiles; j += 2) {
-        step(j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
-        step(j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
+    for (; j + 3 < n_tiles; j += 2) {
+        step(Steady{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+        step(Steady{}, j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
     }
-    if (j < n_tiles) step(j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+    const int left = n_tiles - j;
+    if (left == 3) {
+        step(Steady{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+        step(Penult{}, j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
+        step(LastT{}, j + 2, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+    } else if (left == 2) {
+        step(Penult{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+        step(LastT{}, j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
+    } else {
+        step(LastT{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+    }
 
     const float l_tot = half_swap_sum(l_run0 + l_run1);
     const float inv = 1.0f / l_tot;

@@ -100,6 +100,7 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
     if ((int64_t)B * Tq * h * w > ((int64_t)1 << 31) - 1 || (int64_t)B * S * Tq * h * w > kMaxElems)
         return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: problem too large");
     if (src_sel && n_src < 0) return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: n_src < 0");
+    if (S > 64) return fail(REVISIT_ERR_SHAPE, "reproject_correspondence: more than 64 source frames per problem");
     if (!(finite(eps) && eps >= 0.0f)) return fail(REVISIT_ERR_PARAM, "reproject_correspondence: eps must be finite and >= 0");
     if (B == 0 || Tq == 0 || S == 0) return REVISIT_OK;
     if (!tgt_depth || !tgt_c2w || !tgt_K || !out_uv || !out_idx)

@@ -16,6 +16,10 @@
 // Arithmetic is IEEE double in the order of the definition with
 // contraction disabled; the code and u^ (rounded to fp32 once) are
 // therefore bit-identical to any IEEE evaluation of the same expressions.
+// For the usual p = 2 the kernel is specialised: dividing by 2 or by 4 is
+// the same IEEE result as multiplying by 0.5 or 0.25, so the token-grid
+// intrinsics and the pooling mean cost a multiply instead of a division,
+// and each 2x2 depth block is read as two 8-byte loads.
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -29,33 +33,51 @@ namespace revisit {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kMaxSrcLds = 64;  // source frames per problem
 
 // Mean of the p x p depth block of token (i, j): rows outer, columns inner.
+// P = 2: compile-time 2x2 block; P = 0: runtime p.
+template <int P>
 __device__ __forceinline__ double pooled(const float* __restrict__ d, int Wd, int i, int j, int p) {
-    const float* base = d + (size_t)(i * p) * Wd + (size_t)j * p;
-    double acc = 0.0;
-    bool first = true;
-    for (int a = 0; a < p; ++a) {
-        for (int b = 0; b < p; ++b) {
-            const double x = base[(size_t)a * Wd + b];
-            acc = first ? x : acc + x;
-            first = false;
+    if constexpr (P == 2) {
+        const float2 r0 = *reinterpret_cast<const float2*>(d + (size_t)(2 * i) * Wd + 2 * j);
+        const float2 r1 = *reinterpret_cast<const float2*>(d + (size_t)(2 * i + 1) * Wd + 2 * j);
+        return ((((double)r0.x + (double)r0.y) + (double)r1.x) + (double)r1.y) * 0.25;  // == / 4
+    } else {
+        const float* base = d + (size_t)(i * p) * Wd + (size_t)j * p;
+        double acc = 0.0;
+        bool first = true;
+        for (int a = 0; a < p; ++a) {
+            for (int b = 0; b < p; ++b) {
+                const double x = base[(size_t)a * Wd + b];
+                acc = first ? x : acc + x;
+                first = false;
+            }
         }
+        return acc / (double)(p * p);
     }
-    return acc / (double)(p * p);
 }
 
+// K / p on the token grid (exact multiply by 0.5 when P = 2).
+template <int P>
+__device__ __forceinline__ double per_token(float k, double pd) {
+    if constexpr (P == 2) return (double)k * 0.5;
+    else return (double)k / pd;
+}
+
+template <int P>
 __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const int hw = a.h * a.w;
     const int blocks_per_frame = (hw + kBlock - 1) / kBlock;
-    const int bt = blockIdx.x / blocks_per_frame;  // b * Tq + t
-    const int b = bt / a.Tq;
+    // (problem, target frame) of this block; uniform, kept in scalar registers
+    const int bt = __builtin_amdgcn_readfirstlane(blockIdx.x / blocks_per_frame);  // b * Tq + t
+    const int b = __builtin_amdgcn_readfirstlane(bt / a.Tq);
     const int t = bt - b * a.Tq;
     const int tok = (blockIdx.x - bt * blocks_per_frame) * kBlock + threadIdx.x;
-    if (tok >= hw) return;
-    const int i = tok / a.w;
-    const int j = tok - i * a.w;
-    const int p = a.p;
+    const int tok_c = tok < hw ? tok : hw - 1;  // threads past the frame compute a valid token, store nothing
+    const int i = tok_c / a.w;
+    const int j = tok_c - i * a.w;
+    const int p = P == 2 ? 2 : a.p;
     const int Wd = a.w * p;
     const size_t frame_px = (size_t)hw * p * p;
     const int Lq = a.Tq * hw;
@@ -63,10 +85,10 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
 
     const float* Mt = a.tgt_c2w + (size_t)bt * 16;
     const float* Kt = a.tgt_K + (size_t)bt * 4;
-    const double fxt = (double)Kt[0] / pd, fyt = (double)Kt[1] / pd;
-    const double cxt = (double)Kt[2] / pd, cyt = (double)Kt[3] / pd;
+    const double fxt = per_token<P>(Kt[0], pd), fyt = per_token<P>(Kt[1], pd);
+    const double cxt = per_token<P>(Kt[2], pd), cyt = per_token<P>(Kt[3], pd);
 
-    const double z = pooled(a.tgt_depth + (size_t)bt * frame_px, Wd, i, j, p);
+    const double z = pooled<P>(a.tgt_depth + (size_t)bt * frame_px, Wd, i, j, p);
     const bool defined = isfinite(z) && z > 0.0;
 
     // X_t = z K_t^-1 u~, then R_t X_t + c_t (the source centre comes later)
@@ -82,42 +104,60 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     }
     const double tol = 1.0 + a.eps;
 
+    // Source frames of this problem, converted once per block into LDS as
+    // doubles: R (row-major), c, token-grid (fx, fy, cx, cy); frame index -1 =
+    // no source. The loop below then reads them as broadcasts.
+    __shared__ double src_c[kMaxSrcLds][16];
+    __shared__ int src_f[kMaxSrcLds];
+    for (int s = threadIdx.x; s < a.S; s += kBlock) {
+        int f = b * a.S + s;
+        if (a.src_sel) {
+            f = a.src_sel[(size_t)b * a.S + s];
+            if (f < 0 || f >= a.n_src) f = -1;
+        }
+        src_f[s] = f;
+        if (f >= 0) {
+            const float* Ms = a.src_c2w + (size_t)f * 16;
+            const float* Ks = a.src_K + (size_t)f * 4;
+            for (int r = 0; r < 3; ++r) {
+                for (int c = 0; c < 3; ++c) src_c[s][3 * r + c] = (double)Ms[4 * r + c];
+                src_c[s][9 + r] = (double)Ms[4 * r + 3];
+            }
+            for (int c = 0; c < 4; ++c) src_c[s][12 + c] = per_token<P>(Ks[c], pd);
+        }
+    }
+    __syncthreads();
+    if (tok >= hw) return;
+
     for (int s = 0; s < a.S; ++s) {
         const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
         float2* uv_out = reinterpret_cast<float2*>(a.out_uv) + o;
-        int f;  // source frame index into the src arrays
-        if (a.src_sel) {
-            f = a.src_sel[(size_t)b * a.S + s];
-            if (f < 0 || f >= a.n_src) {
-                *uv_out = make_float2(NAN, NAN);
-                a.out_idx[o] = -5;
-                continue;
-            }
-        } else {
-            f = b * a.S + s;
+        const int f = src_f[s];
+        if (f < 0) {
+            *uv_out = make_float2(NAN, NAN);
+            a.out_idx[o] = -5;
+            continue;
         }
         if (!defined) {
             *uv_out = make_float2(NAN, NAN);
             a.out_idx[o] = -1;
             continue;
         }
-        const float* Ms = a.src_c2w + (size_t)f * 16;
-        const float* Ks = a.src_K + (size_t)f * 4;
+        const double* C = src_c[s];
         // R_t X_t + c_t - c_s
-        const double W0 = Wt[0] - (double)Ms[3];
-        const double W1 = Wt[1] - (double)Ms[7];
-        const double W2 = Wt[2] - (double)Ms[11];
+        const double W0 = Wt[0] - C[9];
+        const double W1 = Wt[1] - C[10];
+        const double W2 = Wt[2] - C[11];
         // X_s = R_s^T (...): component r is column r of R_s dotted with W
-        const double Xs = ((double)Ms[0] * W0 + (double)Ms[4] * W1) + (double)Ms[8] * W2;
-        const double Ys = ((double)Ms[1] * W0 + (double)Ms[5] * W1) + (double)Ms[9] * W2;
-        const double Zs = ((double)Ms[2] * W0 + (double)Ms[6] * W1) + (double)Ms[10] * W2;
+        const double Xs = (C[0] * W0 + C[3] * W1) + C[6] * W2;
+        const double Ys = (C[1] * W0 + C[4] * W1) + C[7] * W2;
+        const double Zs = (C[2] * W0 + C[5] * W1) + C[8] * W2;
         if (!(Zs > 0.0)) {
             *uv_out = make_float2(NAN, NAN);
             a.out_idx[o] = -2;
             continue;
         }
-        const double fxs = (double)Ks[0] / pd, fys = (double)Ks[1] / pd;
-        const double cxs = (double)Ks[2] / pd, cys = (double)Ks[3] / pd;
+        const double fxs = C[12], fys = C[13], cxs = C[14], cys = C[15];
         const double uhx = (fxs * Xs + cxs * Zs) / Zs;
         const double uhy = (fys * Ys + cys * Zs) / Zs;
         *uv_out = make_float2((float)uhx, (float)uhy);
@@ -127,7 +167,7 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
         }
         const int kx = (int)floor(uhx);
         const int ky = (int)floor(uhy);
-        const double Ds = pooled(a.src_depth + (size_t)f * frame_px, Wd, ky, kx, p);
+        const double Ds = pooled<P>(a.src_depth + (size_t)f * frame_px, Wd, ky, kx, p);
         a.out_idx[o] = (Zs <= tol * Ds) ? ky * a.w + kx : -4;
     }
 }
@@ -140,7 +180,11 @@ hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream) {
     const int64_t blocks = (int64_t)((hw + kBlock - 1) / kBlock) * a.B * a.Tq;
     if (blocks > INT32_MAX) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks), block(kBlock);
-    hipLaunchKernelGGL(reproject_kernel, grid, block, 0, stream, a);
+    if (a.p == 2) {
+        hipLaunchKernelGGL(reproject_kernel<2>, grid, block, 0, stream, a);
+    } else {
+        hipLaunchKernelGGL(reproject_kernel<0>, grid, block, 0, stream, a);
+    }
     return hipGetLastError();
 }
 

@@ -91,7 +91,7 @@ def _reproject(L, **kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(h=0), 2), (dict(p=0), 2), (dict(B=-1), 2), (dict(eps=-0.1), 4), (dict(eps=float("nan")), 4),
     (dict(td=NULL), 1), (dict(uv=NULL), 1), (dict(sd=NULL), 1), (dict(sel=FAKE, n_src=-1), 2),
-    (dict(h=1 << 20, w=1 << 20), 2),
+    (dict(h=1 << 20, w=1 << 20), 2), (dict(S=65), 2),
 ])
 def test_reproject_rejects(L, kw, status):
     assert _reproject(L, **kw) == status
