@@ -41,6 +41,28 @@ BENCH_QUERY = 1  # query chunk n = 225: a full top-4 retrieval
 REPROJ_BATCH = 1024
 
 
+def profiled_counters():
+    """HBM traffic of the attention / reprojection kernels as last measured with
+    rocprofv3 (profiles/counters.json), valid only while the kernel sources are
+    unchanged since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    if not os.path.exists(path):
+        return {}
+    with open(path) as f:
+        c = json.load(f)
+    src = os.path.join(ROOT, "paper_2607_21848_amd", "csrc")
+    out = {}
+    for key, fname in (("attention", "attention.hip"), ("reproject", "reproject.hip")):
+        with open(os.path.join(src, fname), "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+        if c.get(f"{key}_sha") == sha:
+            out[key] = c[f"{key}_traffic_bytes"]
+    if "attention" in out and "mfma_busy_fraction" in c:
+        out["mfma_busy_fraction"] = c["mfma_busy_fraction"]
+    return out
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -193,6 +215,7 @@ def main():
     log(f"batched reprojection {rb_ms:.3f} ms: {tokens / (rb_ms * 1e-3):.3e} tokens/s, {rb_gbs:.0f} GB/s algorithmic")
     del bt, buv, bidx
 
+    counters = profiled_counters()
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -219,7 +242,8 @@ def main():
             "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
-            "traffic": None,
+            "traffic": counters.get("attention"),
+            "mfma_busy_profiled": counters.get("mfma_busy_fraction"),
             "flops_per_launch": flops,
             "avg_launch_ms": round(attn_ms, 4),
         },
@@ -235,6 +259,7 @@ def main():
                 "bytes_per_token": bytes_per_token,
                 "achieved_GBs": round(rb_gbs, 1), "peak_GBs": HBM_PEAK_GBS,
                 "frac": round(rb_gbs / HBM_PEAK_GBS, 4), "bound": "hbm",
+                "traffic": counters.get("reproject"),
             },
         },
     }

@@ -374,10 +374,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     const int wave = tid >> 6;
     const int hh = lane >> 5;
     const int n = lane & 31;
-    const int hd = blockIdx.y;
+    // work item = (head, 128-query tile), head-major, each XCD a contiguous range
+    const int n_qt = (a.Lq + 127) / 128;
+    const unsigned item = xcd_item(blockIdx.x, (unsigned)(n_qt * a.H));
+    if (item >= (unsigned)(n_qt * a.H)) return;  // grid padding (uniform, before any barrier)
+    const int hd = (int)item / n_qt;
+    const int qt = (int)item - hd * n_qt;
     const int H = a.H;
     const int Lk = a.Lk;
-    const int q = blockIdx.x * 128 + wave * 32 + n;
+    const int q = qt * 128 + wave * 32 + n;
     const bool q_ok = q < a.Lq;
     const uint16_t* Qg = static_cast<const uint16_t*>(a.q);
     const uint16_t* Kg = static_cast<const uint16_t*>(a.k);
@@ -741,7 +746,7 @@ hipError_t launch_attention_bf16(const AttentionArgs& a, hipStream_t stream) {
     if (a.Lq == 0) return hipSuccess;
     const BiasGeom g = make_geom(a);
     const bool bias_on = a.S > 0 && a.lambda != 0.0f;
-    const dim3 grid((a.Lq + 127) / 128, a.H), block(256);
+    const dim3 grid(xcd_grid((unsigned)(((a.Lq + 127) / 128) * a.H))), block(256);
     if (bias_on) {
         hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e);
     } else {

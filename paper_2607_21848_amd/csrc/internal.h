@@ -8,6 +8,18 @@
 
 namespace revisit {
 
+// Workgroups of a 1-D grid are dealt to the 8 XCDs round-robin (workgroup L
+// runs on XCD L % 8). xcd_item() turns that into "each XCD takes one
+// contiguous range of work items", so the work items that share data (one
+// head's K/V, one problem's source depth) meet in the same L2. The grid is
+// padded to a multiple of 8; the returned item may be >= n_items (nothing to do).
+constexpr int kXcds = 8;
+__host__ __device__ inline unsigned xcd_grid(unsigned n_items) { return (n_items + kXcds - 1) / kXcds * kXcds; }
+__device__ inline unsigned xcd_item(unsigned block, unsigned n_items) {
+    const unsigned per_xcd = (n_items + kXcds - 1) / kXcds;
+    return (block % kXcds) * per_xcd + block / kXcds;
+}
+
 struct RetrieveArgs {
     const float* bank_c2w;
     int32_t n_bank;

@@ -69,11 +69,16 @@ template <int P>
 __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const int hw = a.h * a.w;
     const int blocks_per_frame = (hw + kBlock - 1) / kBlock;
+    // work item = (problem, target frame, token block), problem-major, each XCD a
+    // contiguous range so one problem's source depth stays in one L2
+    const unsigned n_items = (unsigned)(blocks_per_frame * a.B * a.Tq);
+    const int item = (int)__builtin_amdgcn_readfirstlane(xcd_item(blockIdx.x, n_items));
+    if (item >= (int)n_items) return;  // grid padding (uniform, before the barrier)
     // (problem, target frame) of this block; uniform, kept in scalar registers
-    const int bt = __builtin_amdgcn_readfirstlane(blockIdx.x / blocks_per_frame);  // b * Tq + t
+    const int bt = __builtin_amdgcn_readfirstlane(item / blocks_per_frame);  // b * Tq + t
     const int b = __builtin_amdgcn_readfirstlane(bt / a.Tq);
     const int t = bt - b * a.Tq;
-    const int tok = (blockIdx.x - bt * blocks_per_frame) * kBlock + threadIdx.x;
+    const int tok = (item - bt * blocks_per_frame) * kBlock + threadIdx.x;
     const int tok_c = tok < hw ? tok : hw - 1;  // threads past the frame compute a valid token, store nothing
     const int i = tok_c / a.w;
     const int j = tok_c - i * a.w;
@@ -178,8 +183,8 @@ hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream) {
     const int hw = a.h * a.w;
     if (a.B == 0 || a.Tq == 0 || a.S == 0 || hw == 0) return hipSuccess;
     const int64_t blocks = (int64_t)((hw + kBlock - 1) / kBlock) * a.B * a.Tq;
-    if (blocks > INT32_MAX) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)blocks), block(kBlock);
+    if (blocks > INT32_MAX - kXcds) return hipErrorInvalidValue;
+    const dim3 grid(xcd_grid((unsigned)blocks)), block(kBlock);
     if (a.p == 2) {
         hipLaunchKernelGGL(reproject_kernel<2>, grid, block, 0, stream, a);
     } else {
