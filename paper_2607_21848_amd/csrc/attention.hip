@@ -209,7 +209,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
 
 // ---------------------------------------------------------------------------
 // bf16 kernel: v_mfma_f32_32x32x16_bf16, D = 128. 4 waves x 32 queries per
-// workgroup, 64-key tiles (two 32-row MFMA blocks), two workgroups per CU.
+// workgroup, 32-key tiles (one 32-row MFMA block each), two workgroups per CU.
 //
 // Memory path. K and V tiles travel global -> LDS with direct 16-byte loads
 // (no register staging, no VALU). Both stay in their natural [key][d]
@@ -227,7 +227,8 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
 // (MFMA / LDS / VALU), so the exponentials hide behind the matrix work of
 // the same wave, and the second wave of the SIMD fills remaining gaps. Two
 // K and two V buffers; the loads for tiles j+2 (K) and j+1 (V) are issued
-// right after the one barrier of step j.
+// right after the one barrier of step j. Workgroups are mapped XCD-aware
+// (head-major) so the workgroups of one head share an L2.
 //
 // Softmax. exp2 on the raw hardware instruction with scale * log2(e) folded
 // into one FMA, probabilities packed to bf16 pairwise and summed with bf16
