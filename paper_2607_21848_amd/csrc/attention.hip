@@ -252,6 +252,7 @@ constexpr int kTileBytes = kTK * kRowBytes;   // 8 KB per K or V tile
 constexpr float kRescaleSlack = 8.0f;         // lazy rescale: tolerate p up to 2^8
 constexpr int kMaxFramesLds = 1024;           // KV frames (slot table entries) of the bf16 kernel
 constexpr int kMaxGridSide = 256;             // token-grid rows / columns of the bf16 bias tables
+constexpr int kCorrLds = 16;                  // retrieved frames whose correspondences are staged in LDS
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short shortx4 __attribute__((ext_vector_type(4)));
@@ -369,6 +370,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     __shared__ int lds_slot[kBias ? kMaxFramesLds : 1];        // KV frame -> retrieved frame (or -1)
     __shared__ u32x4 lds_col[kBias ? kMaxGridSide : 1];        // key operand, first contraction half, by column
     __shared__ u32x4 lds_row[kBias ? kMaxGridSide : 1];        // key operand, second contraction half, by row
+    __shared__ float2 lds_corr[kBias ? kCorrLds : 1][128];      // centred u^ per (retrieved frame, query)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -448,107 +450,108 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             else lds_row[k] = v;
         }
     }
-    // query-side operands of the frames the next QK tile can touch, by frame
-    int qb_frame[2] = {-1, -1};
-    bf16x8 qb[2] = {as_bf16x8(u32x4{0, 0, 0, 0}), as_bf16x8(u32x4{0, 0, 0, 0})};
+    // Correspondences of this workgroup's 128 queries for the first kCorrLds
+    // retrieved frames, staged once into LDS (centred u^, NaN = rejected), so
+    // that no global load sits in the key loop; frames beyond load on demand.
+    if (kBias) {
+        const int n_s = min(a.S, kCorrLds);
+        for (int e = tid; e < n_s * 128; e += 256) {
+            const int s = e >> 7, qi = e & 127;
+            const int qq = qt * 128 + qi;
+            float2 v = make_float2(NAN, NAN);
+            if (qq < a.Lq) {
+                const size_t o = (size_t)s * a.Lq + qq;
+                if (a.corr_idx[o] >= 0) {
+                    const float2 u = reinterpret_cast<const float2*>(a.corr_uv)[o];
+                    v = make_float2(u.x - g.cx, u.y - g.cy);
+                }
+            }
+            lds_corr[s][qi] = v;
+        }
+    }
+    // query-side bias operand of retrieved frame s for this lane's query
     auto query_operand = [&](int s) -> bf16x8 {
-        u32x4 v = u32x4{0, 0, 0, 0};
-        if (s >= 0 && q_ok) {
+        float ux = NAN, uy = NAN;
+        if (s < kCorrLds) {
+            const float2 v = lds_corr[s][wave * 32 + n];
+            ux = v.x;
+            uy = v.y;
+        } else if (q_ok) {
             const size_t o = (size_t)s * a.Lq + q;
             if (a.corr_idx[o] >= 0) {
                 const float2 u = reinterpret_cast<const float2*>(a.corr_uv)[o];
-                const float ux = u.x - g.cx, uy = u.y - g.cy;
-                uint32_t xh, xm, xl, yh, ym, yl, zh, zm, zl;
-                split3(g.gamma * ux, xh, xm, xl);
-                split3(g.gamma * uy, yh, ym, yl);
-                split3(-g.gamma * (ux * ux + uy * uy), zh, zm, zl);
-                if (hh == 0) v = u32x4{pack2(xh, xm), pack2(xl, one_bf), pack2(one_bf, one_bf), pack2(zh, zm)};
-                else v = u32x4{pack2(yh, ym), pack2(yl, one_bf), pack2(one_bf, one_bf), zl};
+                ux = u.x - g.cx;
+                uy = u.y - g.cy;
             }
+        }
+        u32x4 v = u32x4{0, 0, 0, 0};
+        if (!__builtin_isnan(ux)) {
+            uint32_t xh, xm, xl, yh, ym, yl, zh, zm, zl;
+            split3(g.gamma * ux, xh, xm, xl);
+            split3(g.gamma * uy, yh, ym, yl);
+            split3(-g.gamma * (ux * ux + uy * uy), zh, zm, zl);
+            if (hh == 0) v = u32x4{pack2(xh, xm), pack2(xl, one_bf), pack2(one_bf, one_bf), pack2(zh, zm)};
+            else v = u32x4{pack2(yh, ym), pack2(yl, one_bf), pack2(one_bf, one_bf), zl};
         }
         return as_bf16x8(v);
     };
-    // frame / in-frame offset of the next QK block start (uniform) and of this
-    // lane's key-operand row, both advanced 32 keys per block
+    // the operand of the frame the last biased tile lay in
+    int qcur_f = -1;
+    bf16x8 qcur = as_bf16x8(u32x4{0, 0, 0, 0});
+    // frame and in-frame offset of the next QK tile's first key (uniform)
     int blk_f = 0, blk_t = 0;
-    int lane_t = krow, lane_f = 0;
-    if (kBias) {
-        while (lane_t >= g.hw) {
-            lane_t -= g.hw;
-            ++lane_f;
-        }
-    }
     const float inv_w = 1.0f / (float)g.w;
+    // this lane's key operand for in-frame key position t (< hw)
+    auto key_operand = [&](int t) -> u32x4 {
+        const int ky = (int)(((float)t + 0.5f) * inv_w);
+        const int kx = t - ky * g.w;
+        return hh == 0 ? lds_col[kx] : lds_row[ky];
+    };
 
-    // Bias prelude of a QK block: returns the accumulator start value (the
-    // bias of a second frame when the block straddles two) and sets the key
-    // and query operands of the main bias MFMA.
-    auto bias_prelude = [&](int k0, bf16x8& kv_out, bf16x8& qv_out) -> floatx16 {
+    // Bias of the QK tile starting at key k0, as the accumulator's start value.
+    // Fast path: the 32 keys lie in one frame -> one MFMA (or none for an
+    // unbiased frame). Slow path (a tile that crosses a frame boundary or Lk):
+    // one masked MFMA per retrieved frame the tile touches.
+    auto bias_init = [&](int k0) -> floatx16 {
         floatx16 init = floatx16{0};
-        u32x4 kvA = u32x4{0, 0, 0, 0};
-        bf16x8 qA = as_bf16x8(u32x4{0, 0, 0, 0});
         const int span = min(31, Lk - 1 - k0);
-        // key operand of this lane's row (masked per frame below)
-        u32x4 krow_op = u32x4{0, 0, 0, 0};
-        const bool row_live = krow <= span;
-        if (row_live) {
-            const int ky = (int)(((float)lane_t + 0.5f) * inv_w);
-            const int kx = lane_t - ky * g.w;
-            krow_op = hh == 0 ? lds_col[kx] : lds_row[ky];
-        }
-        for (int i = 0, f = blk_f, fs = -blk_t; fs <= span && f < n_frames; ++i, ++f, fs += g.hw) {
-            const int s = __builtin_amdgcn_readfirstlane(lds_slot[f]);
-            if (s < 0) continue;
-            int slot_i;
-            if (f == qb_frame[0]) {
-                slot_i = 0;
-            } else if (f == qb_frame[1]) {
-                slot_i = 1;
-            } else {
-                // a frame not seen before: it replaces the older entry
-                slot_i = (qb_frame[0] < qb_frame[1]) ? 0 : 1;
-                const bf16x8 nq = query_operand(s);
-                if (slot_i == 0) {
-                    qb[0] = nq;
-                    qb_frame[0] = f;
-                } else {
-                    qb[1] = nq;
-                    qb_frame[1] = f;
+        if (span == 31 && blk_t + 31 < g.hw) {
+            const int s = __builtin_amdgcn_readfirstlane(lds_slot[blk_f]);
+            if (s >= 0) {
+                if (qcur_f != blk_f) {
+                    qcur = query_operand(s);
+                    qcur_f = blk_f;
                 }
+                init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(key_operand(blk_t + krow)), qcur, init, 0, 0, 0);
             }
-            const bf16x8 qv = slot_i == 0 ? qb[0] : qb[1];
-            const u32x4 kv = (row_live && lane_f == f) ? krow_op : u32x4{0, 0, 0, 0};
-            if (i == 0) {
-                kvA = kv;
-                qA = qv;
-            } else {
+        } else {
+            int lane_t = blk_t + krow, lane_f = blk_f;
+            while (lane_t >= g.hw) {
+                lane_t -= g.hw;
+                ++lane_f;
+            }
+            const bool row_live = krow <= span;
+            for (int f = blk_f, fs = -blk_t; fs <= span && f < n_frames; ++f, fs += g.hw) {
+                const int s = __builtin_amdgcn_readfirstlane(lds_slot[f]);
+                if (s < 0) continue;
+                const bf16x8 qv = query_operand(s);
+                u32x4 kv = u32x4{0, 0, 0, 0};
+                if (row_live && lane_f == f) kv = key_operand(lane_t);
                 init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qv, init, 0, 0, 0);
             }
         }
-        kv_out = as_bf16x8(kvA);
-        qv_out = qA;
-        return init;
-    };
-    auto advance_block = [&]() {
         blk_t += 32;
         while (blk_t >= g.hw) {
             blk_t -= g.hw;
             ++blk_f;
         }
-        lane_t += 32;
-        while (lane_t >= g.hw) {
-            lane_t -= g.hw;
-            ++lane_f;
-        }
+        return init;
     };
 
     // QK^T of one 32-key tile from LDS (buffer kt), bias first, into S
     auto qk_tile = [&](const uint8_t* kt, int k0, floatx16& S) {
-        bf16x8 kvb, qvb;
         if constexpr (kBias) {
-            S = bias_prelude(k0, kvb, qvb);
-            advance_block();
-            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kvb, qvb, S, 0, 0, 0);
+            S = bias_init(k0);
         } else {
             S = floatx16{0};
         }
@@ -635,7 +638,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             // LDS reads run ahead of the MFMAs that consume them
             __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
 #pragma unroll
-            for (int i = 0; i < (kBias ? 9 : 8); ++i) {
+            for (int i = 0; i < 8; ++i) {
                 __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(kSchedValu, 6, 0);
