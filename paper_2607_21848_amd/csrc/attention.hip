@@ -249,6 +249,8 @@ constexpr int kD = 128;
 constexpr int kTK = 32;
 constexpr int kRowBytes = kD * 2;             // 256
 constexpr int kTileBytes = kTK * kRowBytes;   // 8 KB per K or V tile
+constexpr int kStages = 3;                    // K / V tiles in flight or resident per ring
+constexpr int kWaitVm0 = 0x0f70;              // s_waitcnt immediate: vmcnt(0), other counters unconstrained
 constexpr float kRescaleSlack = 8.0f;         // lazy rescale: tolerate p up to 2^8
 constexpr int kMaxFramesLds = 1024;           // KV frames (slot table entries) of the bf16 kernel
 constexpr int kMaxGridSide = 256;             // token-grid rows / columns of the bf16 bias tables
@@ -335,16 +337,32 @@ __device__ __forceinline__ TileLoad make_tile_load(size_t row_stride, int hd, in
     return t;
 }
 
-__device__ __forceinline__ void load_tile_lds(const uint16_t* __restrict__ src, uint8_t* lds_tile, int tile0,
+// One direct load of 16 bytes per lane: global (base + voff) -> LDS
+// (lds + 16 * lane). Written as inline asm so that the compiler's own
+// wait-count bookkeeping, which cannot tell the ring slots apart and would
+// drain every load in flight before reading any slot, does not see it; the
+// pipeline orders these loads with explicit vmcnt waits. M0 carries the LDS
+// address and needs one wait state before the load.
+__device__ __forceinline__ void dma_b128(const uint8_t* base, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(lds), "v"(voff), "s"(base)
+                 : "memory", "m0");
+}
+
+// LDS byte address of a pointer into __shared__ memory
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const lds_void*)p;
+}
+
+// lds_wave: LDS byte address of this wave's quarter of the destination tile (uniform)
+__device__ __forceinline__ void load_tile_lds(const uint16_t* __restrict__ src, uint32_t lds_wave, int tile0,
                                               int Lk, size_t row_stride, const TileLoad& tl, int hd, int wave,
                                               int lane) {
     const uint8_t* base = reinterpret_cast<const uint8_t*>(src) + (size_t)tile0 * row_stride * 2;
     if (tile0 + kTK <= Lk) {
 #pragma unroll
-        for (int i = 0; i < kLoadsPerLane; ++i) {
-            __builtin_amdgcn_global_load_lds(base + tl.off[i], (lds_void*)(lds_tile + (wave * kLoadsPerLane + i) * 1024),
-                                             16, 0, 0);
-        }
+        for (int i = 0; i < kLoadsPerLane; ++i) dma_b128(base, tl.off[i], lds_wave + i * 1024);
     } else {
         const int last = Lk - 1 - tile0;
 #pragma unroll
@@ -352,10 +370,20 @@ __device__ __forceinline__ void load_tile_lds(const uint16_t* __restrict__ src, 
             int r, lc;
             tile_chunk(wave, lane, i, r, lc);
             const uint32_t off = (uint32_t)(min(r, last) * (int)(row_stride * 2) + (hd * kD + lc * 8) * 2);
-            __builtin_amdgcn_global_load_lds(base + off, (lds_void*)(lds_tile + (wave * kLoadsPerLane + i) * 1024), 16,
-                                             0, 0);
+            dma_b128(base, off, lds_wave + i * 1024);
         }
     }
+}
+
+// Workgroup barrier with no memory fence. __syncthreads() would also drain
+// every direct global -> LDS load still in flight (they count as LDS writes);
+// the pipeline orders those itself with per-lane vmcnt waits before the
+// barrier. The empty asm statements keep the compiler from moving memory
+// accesses across it.
+__device__ __forceinline__ void wg_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 }
 
 // Scheduling-group masks of the interleave hints.
@@ -363,10 +391,19 @@ constexpr int kSchedMfma = 0x008, kSchedValu = 0x002, kSchedDsRead = 0x100;
 
 template <bool kBias>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, BiasGeom g, float c_log2) {
-    __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[kTileBytes];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[kTileBytes];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[kTileBytes];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[kTileBytes];
+    // Three-slot ring: slot t mod 3 holds K_t in its first half and V_{t-1}
+    // in its second. Step j refills slot j mod 3 (K_{j+3}, V_{j+2}) while it
+    // reads slot j + 1 mod 3 (K_{j+1}, V_j); separate arrays let the compiler
+    // see that those reads never touch the loads still landing.
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_r0[2 * kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_r1[2 * kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_r2[2 * kTileBytes];
+    auto ring = [&](auto slot_tag) -> uint8_t* {
+        constexpr int i = decltype(slot_tag)::value % kStages;
+        if constexpr (i == 0) return lds_r0;
+        else if constexpr (i == 1) return lds_r1;
+        else return lds_r2;
+    };
     __shared__ int lds_slot[kBias ? kMaxFramesLds : 1];        // KV frame -> retrieved frame (or -1)
     __shared__ u32x4 lds_col[kBias ? kMaxGridSide : 1];        // key operand, first contraction half, by column
     __shared__ u32x4 lds_row[kBias ? kMaxGridSide : 1];        // key operand, second contraction half, by row
@@ -395,9 +432,21 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
 
     // start streaming the first tiles before anything else
     const TileLoad tl = make_tile_load(row_stride, hd, wave, lane);
-    load_tile_lds(Kg, lds_k0, 0, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Vg, lds_v0, 0, Lk, row_stride, tl, hd, wave, lane);
-    if (n_tiles > 1) load_tile_lds(Kg, lds_k1, kTK, Lk, row_stride, tl, hd, wave, lane);
+    // K_0, V_0, K_1, V_1, K_2: everything the pipeline's first step expects in
+    // place. With fewer tiles the missing ones repeat the last tile (never read;
+    // loading them anyway keeps these loads free of branches).
+    using R0 = std::integral_constant<int, 0>;
+    using R1 = std::integral_constant<int, 1>;
+    using R2 = std::integral_constant<int, 2>;
+    const int tile1 = min(1, n_tiles - 1) * kTK, tile2 = min(2, n_tiles - 1) * kTK;
+    // this wave's quarter of a K tile in each ring slot (+ kTileBytes: the V tile)
+    const uint32_t wave_off = (uint32_t)__builtin_amdgcn_readfirstlane(wave * kLoadsPerLane * 1024);
+    auto dst = [&](auto slot_tag) -> uint32_t { return lds_addr(ring(slot_tag)) + wave_off; };
+    load_tile_lds(Kg, dst(R0{}), 0, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Vg, dst(R1{}) + kTileBytes, 0, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Kg, dst(R1{}), tile1, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Vg, dst(R2{}) + kTileBytes, tile1, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Kg, dst(R2{}), tile2, Lk, row_stride, tl, hd, wave, lane);
 
     // Q fragments: lane (hh, n) holds Q[q][16 kk + 8 hh .. +8)
     bf16x8 qf[8];
@@ -586,19 +635,35 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     floatx16 Sa, Sb;
     float mx_cur;
 
-    // One pipeline step for tile j: barrier, prefetch of K_{j+2} and V_{j+1},
-    // then softmax + PV of tile j (logits in S_cur, V_j in vcur) while the
-    // logits of tile j + 1 (K_{j+1} in knext) are computed into S_next.
-    // Kinds: 0 = tile j + 1 exists and is not the last, 1 = tile j + 1 is the
-    // last (its keys may run past Lk), 2 = tile j is the last.
-    auto step = [&](auto kind_tag, int j, floatx16& S_cur, floatx16& S_next, const uint8_t* vcur,
-                    const uint8_t* knext, uint8_t* kdst, uint8_t* vdst) {
+    // One pipeline step for tile j. After the barrier, K_{j+3} and V_{j+2} are
+    // loaded into ring slot j mod 3, which held K_j and V_{j-1} (no wave reads
+    // those any more), then softmax + PV of tile j (logits in S_cur) run while
+    // the logits of tile j + 1 are computed into S_next.
+    // P = j mod 6 fixes the ring slots and which of Sa / Sb is current at
+    // compile time. Kinds by the tiles left (d = n_tiles - j): 0 = d >= 4,
+    // 1 = d = 3, 2 = d = 2 (tile j + 1 is the last), 3 = d = 1 (tile j is the last).
+    // Loads issued in step j - 1 may stay in flight: each lane waits only for
+    // those of step j - 2, which carried K_{j+1} and V_j.
+    auto step = [&](auto phase_tag, auto kind_tag, int j) {
+        constexpr int P = decltype(phase_tag)::value;
         constexpr int kind = decltype(kind_tag)::value;
-        constexpr bool has_next = kind != 2;
-        __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this thread's loads of V_j and K_{j+1} have landed
-        __syncthreads();
-        if (j + 2 < n_tiles) load_tile_lds(Kg, kdst, (j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
-        if (j + 1 < n_tiles) load_tile_lds(Vg, vdst, (j + 1) * kTK, Lk, row_stride, tl, hd, wave, lane);
+        constexpr bool has_next = kind != 3;
+        floatx16& S_cur = (P & 1) ? Sb : Sa;
+        floatx16& S_next = (P & 1) ? Sa : Sb;
+        const uint8_t* knext = ring(std::integral_constant<int, P + 1>{});
+        const uint8_t* vcur = knext + kTileBytes;
+        // this lane's loads issued in step j - 1: K_{j+2} if it exists, V_{j+1} if it exists
+        if constexpr (kind <= 1) {
+            __builtin_amdgcn_s_waitcnt(kWaitVm0 + 2 * kLoadsPerLane);
+        } else if constexpr (kind == 2) {
+            __builtin_amdgcn_s_waitcnt(kWaitVm0 + kLoadsPerLane);
+        } else {
+            __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        }
+        wg_barrier();
+        const uint32_t refill = dst(std::integral_constant<int, P>{});
+        if constexpr (kind == 0) load_tile_lds(Kg, refill, (j + 3) * kTK, Lk, row_stride, tl, hd, wave, lane);
+        if constexpr (kind <= 1) load_tile_lds(Vg, refill + kTileBytes, (j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
 
         // row maximum of tile j (reduced during the previous step) and lazy rescale
         const float mx = half_swap_max(mx_cur) * c_log2;
@@ -647,7 +712,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
 
         // region B: PV of tile j on the matrix cores, row maximum of tile j + 1 on the VALU
         float mx_next = -INFINITY;
-        if constexpr (has_next) mx_next = tile_max(std::integral_constant<bool, kind == 1>{}, S_next, nk0);
+        if constexpr (has_next) mx_next = tile_max(std::integral_constant<bool, kind == 2>{}, S_next, nk0);
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -672,33 +737,56 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         }
         mx_cur = mx_next;
     };
-    using Steady = std::integral_constant<int, 0>;
-    using Penult = std::integral_constant<int, 1>;
-    using LastT = std::integral_constant<int, 2>;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    using I4 = std::integral_constant<int, 4>;
+    using I5 = std::integral_constant<int, 5>;
 
     // prologue: logits of tile 0
-    __builtin_amdgcn_s_waitcnt(0x0f70);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
-    qk_tile(lds_k0, 0, Sa);
+    qk_tile(ring(R0{}), 0, Sa);
     mx_cur = n_tiles == 1 ? tile_max(True{}, Sa, 0) : tile_max(False{}, Sa, 0);
 
-    // steady state over pairs of tiles (even tiles: V in v0, K of the next in k1);
-    // then the last one, two or three tiles
+    // steady state in periods of six tiles, while each of them has at least
+    // three more after it
     int j = 0;
-    for (; j + 3 < n_tiles; j += 2) {
-        step(Steady{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
-        step(Steady{}, j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
+    for (; j + 9 <= n_tiles; j += 6) {
+        step(I0{}, I0{}, j);
+        step(I1{}, I0{}, j + 1);
+        step(I2{}, I0{}, j + 2);
+        step(I3{}, I0{}, j + 3);
+        step(I4{}, I0{}, j + 4);
+        step(I5{}, I0{}, j + 5);
     }
+    // the last 1 .. 8 tiles, starting at phase 0: full-loading steps while
+    // d > 3, then the three ending kinds; phases continue modulo 6
     const int left = n_tiles - j;
-    if (left == 3) {
-        step(Steady{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
-        step(Penult{}, j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
-        step(LastT{}, j + 2, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
-    } else if (left == 2) {
-        step(Penult{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
-        step(LastT{}, j + 1, Sb, Sa, lds_v1, lds_k0, lds_k1, lds_v0);
-    } else {
-        step(LastT{}, j, Sa, Sb, lds_v0, lds_k1, lds_k0, lds_v1);
+    auto ending = [&](auto p_tag) {
+        constexpr int P = decltype(p_tag)::value;
+        step(std::integral_constant<int, P % 6>{}, I1{}, n_tiles - 3);
+        step(std::integral_constant<int, (P + 1) % 6>{}, I2{}, n_tiles - 2);
+        step(std::integral_constant<int, (P + 2) % 6>{}, I3{}, n_tiles - 1);
+    };
+    if (left >= 4) step(I0{}, I0{}, j);
+    if (left >= 5) step(I1{}, I0{}, j + 1);
+    if (left >= 6) step(I2{}, I0{}, j + 2);
+    if (left >= 7) step(I3{}, I0{}, j + 3);
+    if (left >= 8) step(I4{}, I0{}, j + 4);
+    switch (left) {
+        case 1: step(I0{}, I3{}, j); break;
+        case 2:
+            step(I0{}, I2{}, j);
+            step(I1{}, I3{}, j + 1);
+            break;
+        case 3: ending(I0{}); break;
+        case 4: ending(I1{}); break;
+        case 5: ending(I2{}); break;
+        case 6: ending(I3{}); break;
+        case 7: ending(I4{}); break;
+        default: ending(I5{}); break;
     }
 
     const float l_tot = half_swap_sum(l_run0 + l_run1);
