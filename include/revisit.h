@@ -19,8 +19,10 @@
  * --------------------------------------
  * - Every array argument is a DEVICE pointer owned by the caller and must
  *   stay valid until the work queued on `stream` has completed. Outputs must
- *   not alias inputs. The library allocates no memory and keeps no state
- *   other than a per-thread last-error string.
+ *   not alias inputs. State kept by the library: a per-thread last-error
+ *   string, the setting of rc_set_attention_key_parts(), and the bf16
+ *   attention workspace described at biased_chunk_attention (the only
+ *   device memory it allocates).
  * - Calls are asynchronous on `stream` (NULL = the default stream).
  * - Arguments are validated on the host before anything is queued: on a
  *   non-zero status nothing has been enqueued and rc_last_error() says why.
@@ -185,6 +187,18 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
  *   (REVISIT_ERR_SHAPE otherwise).
  *
  * Lq == 0 is valid (nothing to do).
+ *
+ * bf16 work split: each (head, 128-query tile) item runs on one workgroup,
+ * or, when the number of items leaves part of the GPU idle in the last round
+ * of workgroups, its keys are cut into P equal parts that run on P
+ * workgroups (P chosen per call, or set by rc_set_attention_key_parts()).
+ * With P > 1 a second kernel on the same stream merges the parts from fp32
+ * partial results in a library-owned device workspace (items * P * 66 KiB;
+ * 234 MiB for 444 items in 8 parts): one block per (device, stream),
+ * allocated with hipMalloc on the first call that needs it and grown by later
+ * calls that need more (after synchronising that stream). Calls queued on one
+ * stream share its block in order; calls on different streams never share
+ * one. A failed allocation returns REVISIT_ERR_LAUNCH with nothing enqueued.
  */
 int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
                            float* lse, int32_t dtype,
@@ -193,6 +207,17 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
                            const float* corr_uv, const int32_t* corr_idx, int32_t S,
                            float softmax_scale, float lambda, float sigma,
                            hipStream_t stream);
+
+/*
+ * rc_set_attention_key_parts -- tuning knob of the bf16 attention work split
+ * (not part of the method): the number of key parts P that later calls of
+ * biased_chunk_attention cut each item into, process-wide (at most one part
+ * per 32-key tile); 0 (the initial value) = chosen per call from the shape
+ * and the compute units of the current device. Any value gives the same
+ * results up to the fp32 rounding of the merge. Returns REVISIT_ERR_PARAM for
+ * values outside [0, 64].
+ */
+int rc_set_attention_key_parts(int32_t parts);
 
 #ifdef __cplusplus
 }

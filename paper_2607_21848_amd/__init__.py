@@ -25,7 +25,8 @@ import torch
 from . import _lib
 from ._lib import BF16, F32, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
 
-__all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "RevisitError", "lib"]
+__all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "set_attention_key_parts",
+           "RevisitError", "lib"]
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -172,3 +173,10 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
                                       softmax_scale, lam, sigma, _stream(dev))
     _lib.check("biased_chunk_attention", st)
     return o, lse
+
+
+def set_attention_key_parts(parts: int) -> None:
+    """Key parts P that later bf16 attention calls cut each (head, query
+    tile) into, process-wide (0 = chosen per call). A tuning knob: results
+    agree up to the fp32 rounding of the partial-result merge for every P."""
+    _lib.check("rc_set_attention_key_parts", lib().rc_set_attention_key_parts(int(parts)))

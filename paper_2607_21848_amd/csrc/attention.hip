@@ -36,6 +36,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "internal.h"
@@ -256,6 +257,16 @@ constexpr int kMaxFramesLds = 1024;           // KV frames (slot table entries) 
 constexpr int kMaxGridSide = 256;             // token-grid rows / columns of the bf16 bias tables
 constexpr int kCorrLds = 16;                  // retrieved frames whose correspondences are staged in LDS
 
+// Key split: the key tiles of every item (head, 128-query tile) are cut into
+// `parts` equal ranges, part p = tiles [p n / parts, (p + 1) n / parts). One
+// workgroup per (item, part); with parts > 1 each leaves its unnormalised
+// result in partial slot item * parts + p for attn_merge_kernel.
+struct KeySplit {
+    int32_t parts;
+    float* part;
+};
+constexpr int kPartFloats = 128 * kD + 2 * 128;  // O [128 queries][kD], then m [128], l [128]
+
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
@@ -341,13 +352,17 @@ __device__ __forceinline__ TileLoad make_tile_load(size_t row_stride, int hd, in
 // (lds + 16 * lane). Written as inline asm so that the compiler's own
 // wait-count bookkeeping, which cannot tell the ring slots apart and would
 // drain every load in flight before reading any slot, does not see it; the
-// pipeline orders these loads with explicit vmcnt waits. M0 carries the LDS
-// address and needs one wait state before the load.
+// pipeline orders these loads with explicit vmcnt waits (extra loads the
+// compiler issues can only make those waits stricter: loads retire in order).
+// M0 carries the LDS address and needs one wait state before the load. M0 is
+// a reserved register that the compiler never allocates, and nothing else in
+// these kernels reads it (it feeds only LDS-DMA, GWS and message
+// instructions), so the asm need not preserve it.
 __device__ __forceinline__ void dma_b128(const uint8_t* base, uint32_t voff, uint32_t lds) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :
                  : "s"(lds), "v"(voff), "s"(base)
-                 : "memory", "m0");
+                 : "memory");
 }
 
 // LDS byte address of a pointer into __shared__ memory
@@ -390,7 +405,7 @@ __device__ __forceinline__ void wg_barrier() {
 constexpr int kSchedMfma = 0x008, kSchedValu = 0x002, kSchedDsRead = 0x100;
 
 template <bool kBias>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, BiasGeom g, float c_log2) {
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, BiasGeom g, float c_log2, KeySplit ks) {
     // Three-slot ring: slot t mod 3 holds K_t in its first half and V_{t-1}
     // in its second. Step j refills slot j mod 3 (K_{j+3}, V_{j+2}) while it
     // reads slot j + 1 mod 3 (K_{j+1}, V_j); separate arrays let the compiler
@@ -414,48 +429,32 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     const int wave = tid >> 6;
     const int hh = lane >> 5;
     const int n = lane & 31;
-    // work item = (head, 128-query tile), head-major, each XCD a contiguous range
+    // Work unit = (head, key part, 128-query tile), in that order of
+    // significance, so that the workgroups running together on one XCD read
+    // the same keys and values; each XCD takes a contiguous range of units.
     const int n_qt = (a.Lq + 127) / 128;
-    const unsigned item = xcd_item(blockIdx.x, (unsigned)(n_qt * a.H));
-    if (item >= (unsigned)(n_qt * a.H)) return;  // grid padding (uniform, before any barrier)
-    const int hd = (int)item / n_qt;
-    const int qt = (int)item - hd * n_qt;
-    const int H = a.H;
     const int Lk = a.Lk;
-    const int q = qt * 128 + wave * 32 + n;
-    const bool q_ok = q < a.Lq;
+    const int n_tiles = (Lk + kTK - 1) / kTK;
+    const unsigned n_units = (unsigned)(n_qt * a.H * ks.parts);
+    const unsigned unit = xcd_item(blockIdx.x, n_units);
+    if (unit >= n_units) return;  // grid padding (uniform, before any barrier)
+    const int qt = (int)(unit % (unsigned)n_qt);
+    const int hp = (int)(unit / (unsigned)n_qt);
+    const int hd = hp / ks.parts;
+    const int kp = hp - hd * ks.parts;
+    const int t0 = (int)((int64_t)kp * n_tiles / ks.parts);
+    const int nt = (int)((int64_t)(kp + 1) * n_tiles / ks.parts) - t0;
+    const int H = a.H;
     const uint16_t* Qg = static_cast<const uint16_t*>(a.q);
     const uint16_t* Kg = static_cast<const uint16_t*>(a.k);
     const uint16_t* Vg = static_cast<const uint16_t*>(a.v);
     const size_t row_stride = (size_t)H * kD;  // elements between consecutive tokens
-    const int n_tiles = (Lk + kTK - 1) / kTK;
-
-    // start streaming the first tiles before anything else
-    const TileLoad tl = make_tile_load(row_stride, hd, wave, lane);
-    // K_0, V_0, K_1, V_1, K_2: everything the pipeline's first step expects in
-    // place. With fewer tiles the missing ones repeat the last tile (never read;
-    // loading them anyway keeps these loads free of branches).
     using R0 = std::integral_constant<int, 0>;
     using R1 = std::integral_constant<int, 1>;
     using R2 = std::integral_constant<int, 2>;
-    const int tile1 = min(1, n_tiles - 1) * kTK, tile2 = min(2, n_tiles - 1) * kTK;
     // this wave's quarter of a K tile in each ring slot (+ kTileBytes: the V tile)
     const uint32_t wave_off = (uint32_t)__builtin_amdgcn_readfirstlane(wave * kLoadsPerLane * 1024);
     auto dst = [&](auto slot_tag) -> uint32_t { return lds_addr(ring(slot_tag)) + wave_off; };
-    load_tile_lds(Kg, dst(R0{}), 0, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Vg, dst(R1{}) + kTileBytes, 0, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Kg, dst(R1{}), tile1, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Vg, dst(R2{}) + kTileBytes, tile1, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Kg, dst(R2{}), tile2, Lk, row_stride, tl, hd, wave, lane);
-
-    // Q fragments: lane (hh, n) holds Q[q][16 kk + 8 hh .. +8)
-    bf16x8 qf[8];
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-        u32x4 v = u32x4{0, 0, 0, 0};
-        if (q_ok) v = *reinterpret_cast<const u32x4*>(Qg + (size_t)q * row_stride + (size_t)hd * kD + 16 * kk + 8 * hh);
-        qf[kk] = as_bf16x8(v);
-    }
 
     // LDS byte offsets (within a tile) of this lane's operand reads
     const int krow = perm_row(n);
@@ -499,9 +498,35 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             else lds_row[k] = v;
         }
     }
-    // Correspondences of this workgroup's 128 queries for the first kCorrLds
-    // retrieved frames, staged once into LDS (centred u^, NaN = rejected), so
-    // that no global load sits in the key loop; frames beyond load on demand.
+    const float inv_w = 1.0f / (float)g.w;
+
+    const int q = qt * 128 + wave * 32 + n;
+    const bool q_ok = q < a.Lq;
+
+    // start streaming the first tiles: K_0, V_0, K_1, V_1, K_2 of the key
+    // part, everything its first step expects in place. With fewer tiles the missing
+    // ones repeat the last tile (never read; loading them anyway keeps these
+    // loads free of branches).
+    const TileLoad tl = make_tile_load(row_stride, hd, wave, lane);
+    const int tile0 = t0 * kTK, tile1 = (t0 + min(1, nt - 1)) * kTK, tile2 = (t0 + min(2, nt - 1)) * kTK;
+    load_tile_lds(Kg, dst(R0{}), tile0, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Vg, dst(R1{}) + kTileBytes, tile0, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Kg, dst(R1{}), tile1, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Vg, dst(R2{}) + kTileBytes, tile1, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Kg, dst(R2{}), tile2, Lk, row_stride, tl, hd, wave, lane);
+
+    // Q fragments: lane (hh, n) holds Q[q][16 kk + 8 hh .. +8)
+    bf16x8 qf[8];
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+        u32x4 v = u32x4{0, 0, 0, 0};
+        if (q_ok) v = *reinterpret_cast<const u32x4*>(Qg + (size_t)q * row_stride + (size_t)hd * kD + 16 * kk + 8 * hh);
+        qf[kk] = as_bf16x8(v);
+    }
+
+    // Correspondences of the 128 queries for the first kCorrLds
+    // retrieved frames, staged into LDS (centred u^, NaN = rejected), so that
+    // no global load sits in the key loop; frames beyond load on demand.
     if (kBias) {
         const int n_s = min(a.S, kCorrLds);
         for (int e = tid; e < n_s * 128; e += 256) {
@@ -548,8 +573,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     int qcur_f = -1;
     bf16x8 qcur = as_bf16x8(u32x4{0, 0, 0, 0});
     // frame and in-frame offset of the next QK tile's first key (uniform)
-    int blk_f = 0, blk_t = 0;
-    const float inv_w = 1.0f / (float)g.w;
+    int blk_f = tile0 / g.hw, blk_t = tile0 - blk_f * g.hw;
     // this lane's key operand for in-frame key position t (< hw)
     auto key_operand = [&](int t) -> u32x4 {
         const int ky = (int)(((float)t + 0.5f) * inv_w);
@@ -662,8 +686,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         }
         wg_barrier();
         const uint32_t refill = dst(std::integral_constant<int, P>{});
-        if constexpr (kind == 0) load_tile_lds(Kg, refill, (j + 3) * kTK, Lk, row_stride, tl, hd, wave, lane);
-        if constexpr (kind <= 1) load_tile_lds(Vg, refill + kTileBytes, (j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
+        if constexpr (kind == 0) load_tile_lds(Kg, refill, (t0 + j + 3) * kTK, Lk, row_stride, tl, hd, wave, lane);
+        if constexpr (kind <= 1) load_tile_lds(Vg, refill + kTileBytes, (t0 + j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
 
         // row maximum of tile j (reduced during the previous step) and lazy rescale
         const float mx = half_swap_max(mx_cur) * c_log2;
@@ -678,7 +702,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         }
 
         // region A: QK of tile j + 1 on the matrix cores, probabilities of tile j on the VALU
-        const int nk0 = (j + 1) * kTK;
+        const int nk0 = (t0 + j + 1) * kTK;
         if constexpr (has_next) qk_tile(knext, nk0, S_next);
         bf16x8 pf[2];
 #pragma unroll
@@ -747,13 +771,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // prologue: logits of tile 0
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
-    qk_tile(ring(R0{}), 0, Sa);
-    mx_cur = n_tiles == 1 ? tile_max(True{}, Sa, 0) : tile_max(False{}, Sa, 0);
+    qk_tile(ring(R0{}), tile0, Sa);
+    mx_cur = t0 + 1 == n_tiles ? tile_max(True{}, Sa, tile0) : tile_max(False{}, Sa, tile0);
 
     // steady state in periods of six tiles, while each of them has at least
     // three more after it
     int j = 0;
-    for (; j + 9 <= n_tiles; j += 6) {
+    for (; j + 9 <= nt; j += 6) {
         step(I0{}, I0{}, j);
         step(I1{}, I0{}, j + 1);
         step(I2{}, I0{}, j + 2);
@@ -763,12 +787,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     }
     // the last 1 .. 8 tiles, starting at phase 0: full-loading steps while
     // d > 3, then the three ending kinds; phases continue modulo 6
-    const int left = n_tiles - j;
+    const int left = nt - j;
     auto ending = [&](auto p_tag) {
         constexpr int P = decltype(p_tag)::value;
-        step(std::integral_constant<int, P % 6>{}, I1{}, n_tiles - 3);
-        step(std::integral_constant<int, (P + 1) % 6>{}, I2{}, n_tiles - 2);
-        step(std::integral_constant<int, (P + 2) % 6>{}, I3{}, n_tiles - 1);
+        step(std::integral_constant<int, P % 6>{}, I1{}, nt - 3);
+        step(std::integral_constant<int, (P + 1) % 6>{}, I2{}, nt - 2);
+        step(std::integral_constant<int, (P + 2) % 6>{}, I3{}, nt - 1);
     };
     if (left >= 4) step(I0{}, I0{}, j);
     if (left >= 5) step(I1{}, I0{}, j + 1);
@@ -790,20 +814,41 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     }
 
     const float l_tot = half_swap_sum(l_run0 + l_run1);
-    const float inv = 1.0f / l_tot;
-    if (q_ok) {
-        uint16_t* Og = static_cast<uint16_t*>(a.o) + (size_t)q * row_stride + (size_t)hd * kD;
+    if (t0 == 0 && nt == n_tiles) {
+        // the whole key range: normalise and store
+        const float inv = 1.0f / l_tot;
+        if (q_ok) {
+            uint16_t* Og = static_cast<uint16_t*>(a.o) + (size_t)q * row_stride + (size_t)hd * kD;
+#pragma unroll
+            for (int db = 0; db < 4; ++db) {
+#pragma unroll
+                for (int gi = 0; gi < 4; ++gi) {
+                    const int d = 32 * db + 8 * gi + 4 * hh;
+                    const uint32_t w0 = cvt_pk_bf16(O[db][4 * gi] * inv, O[db][4 * gi + 1] * inv);
+                    const uint32_t w1 = cvt_pk_bf16(O[db][4 * gi + 2] * inv, O[db][4 * gi + 3] * inv);
+                    *reinterpret_cast<uint2*>(Og + d) = make_uint2(w0, w1);
+                }
+            }
+            if (a.lse && hh == 0) a.lse[(size_t)hd * a.Lq + q] = (m_run + log2f(l_tot)) * kLn2;
+        }
+    } else {
+        // one part of the key range: unnormalised O with its running max and
+        // sum, merged by attn_merge_kernel
+        float* part = ks.part + ((size_t)(hd * n_qt + qt) * ks.parts + kp) * kPartFloats;
+        const int qi = wave * 32 + n;
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
 #pragma unroll
             for (int gi = 0; gi < 4; ++gi) {
                 const int d = 32 * db + 8 * gi + 4 * hh;
-                const uint32_t w0 = cvt_pk_bf16(O[db][4 * gi] * inv, O[db][4 * gi + 1] * inv);
-                const uint32_t w1 = cvt_pk_bf16(O[db][4 * gi + 2] * inv, O[db][4 * gi + 3] * inv);
-                *reinterpret_cast<uint2*>(Og + d) = make_uint2(w0, w1);
+                *reinterpret_cast<float4*>(part + qi * kD + d) =
+                    make_float4(O[db][4 * gi], O[db][4 * gi + 1], O[db][4 * gi + 2], O[db][4 * gi + 3]);
             }
         }
-        if (a.lse && hh == 0) a.lse[(size_t)hd * a.Lq + q] = (m_run + log2f(l_tot)) * kLn2;
+        if (hh == 0) {
+            part[128 * kD + qi] = m_run;
+            part[128 * kD + 128 + qi] = l_tot;
+        }
     }
 }
 
@@ -834,17 +879,81 @@ hipError_t launch_attention_f32(const AttentionArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_attention_bf16(const AttentionArgs& a, hipStream_t stream) {
+namespace {
+
+// O = sum_p 2^(m_p - M) O_p / sum_p 2^(m_p - M) l_p over the key parts p of
+// an item, M = max_p m_p (logits in log2 units). A workgroup merges 8 queries
+// of one item: thread t takes query t / 32 and head dims 4 (t % 32) .. +3, so
+// that each wave reads two whole 512-byte partial rows per load.
+constexpr int kMergeQueries = 8;
+
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttentionArgs a, KeySplit ks) {
+    const int n_qt = (a.Lq + 127) / 128;
+    const int item = blockIdx.x / (128 / kMergeQueries);
+    const int qi = (blockIdx.x % (128 / kMergeQueries)) * kMergeQueries + (threadIdx.x >> 5);
+    const int d = 4 * (threadIdx.x & 31);
+    const int hd = item / n_qt;
+    const int q = (item - hd * n_qt) * 128 + qi;
+    if (q >= a.Lq) return;
+    const float* base = ks.part + (size_t)item * ks.parts * kPartFloats;
+    float M = -INFINITY;
+    for (int p = 0; p < ks.parts; ++p) M = fmaxf(M, base[(size_t)p * kPartFloats + 128 * kD + qi]);
+    float L = 0.0f;
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int p = 0; p < ks.parts; ++p) {
+        const float* P = base + (size_t)p * kPartFloats;
+        const float c = __builtin_amdgcn_exp2f(P[128 * kD + qi] - M);
+        L = fmaf(c, P[128 * kD + 128 + qi], L);
+        const float4 v = *reinterpret_cast<const float4*>(P + qi * kD + d);
+        acc = make_float4(fmaf(c, v.x, acc.x), fmaf(c, v.y, acc.y), fmaf(c, v.z, acc.z), fmaf(c, v.w, acc.w));
+    }
+    const float inv = 1.0f / L;
+    uint16_t* Og = static_cast<uint16_t*>(a.o) + (size_t)q * a.H * kD + (size_t)hd * kD + d;
+    *reinterpret_cast<uint2*>(Og) = make_uint2(cvt_pk_bf16(acc.x * inv, acc.y * inv), cvt_pk_bf16(acc.z * inv, acc.w * inv));
+    if (a.lse && d == 0) a.lse[(size_t)hd * a.Lq + q] = (M + log2f(L)) * kLn2;
+}
+
+}  // namespace
+
+int32_t attention_bf16_key_parts(const AttentionArgs& a, int32_t slots) {
+    // Smallest number of key parts whose workgroups fill the last round of
+    // `slots` resident workgroups to 97 % or more, with parts of at least
+    // kMinTiles key tiles; one part (no merge pass) when none does.
+    constexpr int kMinTiles = 128, kMaxParts = 8;
+    const int64_t items = (int64_t)((a.Lq + 127) / 128) * a.H;
+    const int n_tiles = (a.Lk + kTK - 1) / kTK;
+    for (int p = 1; p <= kMaxParts && (p == 1 || n_tiles / p >= kMinTiles); ++p) {
+        const int64_t units = items * p;
+        const int64_t rounds = (units + slots - 1) / slots;
+        if ((double)units >= 0.97 * (double)(rounds * slots)) return p;
+    }
+    return 1;
+}
+
+size_t attention_bf16_workspace_bytes(const AttentionArgs& a, int32_t parts) {
+    if (parts <= 1) return 0;
+    const int64_t items = (int64_t)((a.Lq + 127) / 128) * a.H;
+    return (size_t)items * parts * kPartFloats * sizeof(float);
+}
+
+hipError_t launch_attention_bf16(const AttentionArgs& a, int32_t parts, float* workspace, hipStream_t stream) {
     if (a.Lq == 0) return hipSuccess;
     const BiasGeom g = make_geom(a);
     const bool bias_on = a.S > 0 && a.lambda != 0.0f;
-    const dim3 grid(xcd_grid((unsigned)(((a.Lq + 127) / 128) * a.H))), block(256);
+    const unsigned items = (unsigned)(((a.Lq + 127) / 128) * a.H);
+    const KeySplit ks{parts, workspace};
+    const dim3 grid(xcd_grid(items * (unsigned)parts)), block(256);
     if (bias_on) {
-        hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e);
+        hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e, ks);
     } else {
-        hipLaunchKernelGGL(attn_bf16_kernel<false>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e);
+        hipLaunchKernelGGL(attn_bf16_kernel<false>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e, ks);
     }
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && parts > 1) {
+        hipLaunchKernelGGL(attn_merge_kernel, dim3(items * (128 / kMergeQueries)), block, 0, stream, a, ks);
+        e = hipGetLastError();
+    }
+    return e;
 }
 
 }  // namespace revisit

@@ -1,11 +1,14 @@
-// C entry points of librevisit: argument validation on the host, then one
-// kernel launch each on the caller's stream. Nothing is allocated; the only
-// state is a per-thread last-error string.
+// C entry points of librevisit: argument validation on the host, then the
+// kernel launches on the caller's stream. State: a per-thread last-error
+// string, the bf16 attention key-part setting, and the attention workspace
+// (workspace.cpp).
 
 #include <math.h>
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
+
+#include <atomic>
 
 #include <hip/hip_runtime.h>
 
@@ -35,6 +38,10 @@ bool aligned(const void* ptr, uintptr_t bytes) { return ((uintptr_t)ptr % bytes)
 
 constexpr int64_t kMaxElems = (int64_t)1 << 40;
 constexpr int kMaxFrames = 1024;
+constexpr int kMaxKeyParts = 64;
+
+// key parts of the bf16 attention kernel; 0 = chosen per call
+std::atomic<int> g_attention_key_parts{0};
 
 }  // namespace
 
@@ -149,6 +156,9 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     if (Lk / hw > kMaxFrames) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: more than %d KV frames", kMaxFrames);
     if ((int64_t)Lk * H * D > kMaxElems || (int64_t)Lq * H * D > kMaxElems || (int64_t)S * Lq > kMaxElems)
         return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: problem too large");
+    // (head, key part, 128-query tile) workgroups of the bf16 kernel: a 32-bit count
+    if (((int64_t)Lq + 127) / 128 * H * kMaxKeyParts > ((int64_t)1 << 31))
+        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: problem too large");
     if (!(finite(softmax_scale) && softmax_scale > 0.0f))
         return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: softmax_scale must be finite and > 0");
     if (!(finite(sigma) && sigma > 0.0f)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: sigma must be finite and > 0");
@@ -183,9 +193,27 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     a.softmax_scale = softmax_scale;
     a.lambda = lambda;
     a.sigma = sigma;
-    const hipError_t e = dtype == REVISIT_BF16 ? revisit::launch_attention_bf16(a, stream)
-                                               : revisit::launch_attention_f32(a, stream);
-    return launched(e, "biased_chunk_attention");
+    if (dtype == REVISIT_F32) return launched(revisit::launch_attention_f32(a, stream), "biased_chunk_attention");
+    if (Lq == 0) return REVISIT_OK;
+    int32_t parts = g_attention_key_parts.load();
+    if (parts == 0) {
+        int cus = 0;
+        const hipError_t e = revisit::device_compute_units(&cus);
+        if (e != hipSuccess) return launched(e, "biased_chunk_attention");
+        parts = revisit::attention_bf16_key_parts(a, 2 * cus);  // two resident workgroups per compute unit
+    }
+    parts = parts < (Lk + 31) / 32 ? parts : (Lk + 31) / 32;  // at least one key tile per part
+    void* ws = nullptr;
+    const hipError_t e = revisit::stream_workspace(stream, revisit::attention_bf16_workspace_bytes(a, parts), &ws);
+    if (e != hipSuccess) return fail(REVISIT_ERR_LAUNCH, "biased_chunk_attention: workspace: %s", hipGetErrorString(e));
+    return launched(revisit::launch_attention_bf16(a, parts, static_cast<float*>(ws), stream), "biased_chunk_attention");
+}
+
+int rc_set_attention_key_parts(int32_t parts) {
+    if (parts < 0 || parts > kMaxKeyParts)
+        return fail(REVISIT_ERR_PARAM, "rc_set_attention_key_parts: %d outside [0, %d]", parts, kMaxKeyParts);
+    g_attention_key_parts.store(parts);
+    return REVISIT_OK;
 }
 
 }  // extern "C"

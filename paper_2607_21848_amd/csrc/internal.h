@@ -4,6 +4,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace revisit {
@@ -65,7 +66,20 @@ struct AttentionArgs {
     int32_t S;  // 0 = bias off
     float softmax_scale, lambda, sigma;
 };
-hipError_t launch_attention_bf16(const AttentionArgs& a, hipStream_t stream);
 hipError_t launch_attention_f32(const AttentionArgs& a, hipStream_t stream);
+
+// bf16 attention: the key tiles of each (head, 128-query tile) item are cut
+// into `parts` equal ranges, one workgroup each; with parts > 1 a second
+// kernel merges the partial results kept in `workspace`
+// (attention_bf16_workspace_bytes). attention_bf16_key_parts picks the
+// number of parts that fills `slots` resident workgroups best.
+int32_t attention_bf16_key_parts(const AttentionArgs& a, int32_t slots);
+size_t attention_bf16_workspace_bytes(const AttentionArgs& a, int32_t parts);
+hipError_t launch_attention_bf16(const AttentionArgs& a, int32_t parts, float* workspace, hipStream_t stream);
+
+// Library-owned device memory of `bytes` for work queued on `stream` of the
+// current device (see workspace.cpp); compute units of the current device.
+hipError_t stream_workspace(hipStream_t stream, size_t bytes, void** out);
+hipError_t device_compute_units(int* cus);
 
 }  // namespace revisit

@@ -30,7 +30,7 @@ def declared_functions():
 def test_header_declares_the_three_stages():
     names = declared_functions()
     for n in ("retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "rc_status_string",
-              "rc_last_error"):
+              "rc_last_error", "rc_set_attention_key_parts"):
         assert n in names
 
 
@@ -125,3 +125,9 @@ def test_attention_bias_pointers_optional_when_off(L):
     # S = 0 or lambda = 0 with NULL map pointers passes validation; Lq = 0 then returns before any launch
     assert _attention(L, Lq=0, S=0, uv=NULL, idx=NULL, slot=NULL) == 0
     assert _attention(L, Lq=0, lam=0.0, uv=NULL, idx=NULL, slot=NULL) == 0
+
+
+@pytest.mark.parametrize("n,status", [(-1, 4), (65, 4), (7, 0), (64, 0), (0, 0)])
+def test_attention_key_parts_knob(L, n, status):
+    assert L.rc_set_attention_key_parts(n) == status
+    L.rc_set_attention_key_parts(0)

@@ -349,6 +349,45 @@ def test_attention_constant_values_and_single_key(dtype):
     assert (o.float() - 0.75).abs().max().item() <= (4e-6 if dtype == "f32" else 4e-3)
 
 
+_SPLIT_CASE = {}
+
+
+def _split_case():
+    """Lq = 300 (three query tiles, the last ragged), Lk = 40 frames of 7 x 10
+    tokens (87.5 key tiles), two heads: 6 items of 88 key tiles."""
+    if not _SPLIT_CASE:
+        rng = np.random.default_rng(21)
+        Lq, Lk, H, D, h, w, S = 300, 40 * 70, 2, 128, 7, 10, 3
+        q, k, v, slot, uv, idx = _synthetic(rng, Lq, Lk, H, D, h, w, S, "bf16")
+        Oo, Lo = OA.biased_attention(q, k, v, slot, uv, idx, h, w, 1.0 / math.sqrt(D), 1.0, 2.0)
+        _SPLIT_CASE.update(dict(args=(q, k, v, slot, uv, idx), hw=(h, w), D=D, ref=(Oo, Lo)))
+    return _SPLIT_CASE
+
+
+@pytest.mark.parametrize("parts", [1, 2, 3, 7, 64])
+def test_attention_bf16_key_parts(parts):
+    """The bf16 key split at forced part counts on 88 key tiles: 1 (no
+    merge), 2 and 3 (parts that start inside KV frames; the last part holds
+    the ragged key tile), 7, and 64 (parts of one or two tiles)."""
+    c = _split_case()
+    q, k, v, slot, uv, idx = c["args"]
+    h, w = c["hw"]
+    Oo, Lo = c["ref"]
+    try:
+        rv.set_attention_key_parts(parts)
+        o, lse = rv.biased_chunk_attention(dev(q, torch.bfloat16), dev(k, torch.bfloat16), dev(v, torch.bfloat16),
+                                           dev(slot), dev(uv), dev(idx), h=h, w=w,
+                                           softmax_scale=1.0 / math.sqrt(c["D"]), lam=1.0, sigma=2.0)
+        torch.cuda.synchronize()
+    finally:
+        rv.set_attention_key_parts(0)
+    err = np.abs(host(o) - Oo).max()
+    lerr = np.abs(host(lse) - Lo).max()
+    print(f"bf16 keys in {parts} parts: max|dO|={err:.3e} max|dLSE|={lerr:.3e}")
+    assert np.isfinite(host(o)).all()
+    assert err <= BF16_TOL and lerr <= LSE_BF16_TOL
+
+
 def test_empty_query_chunk_is_noop():
     q = torch.empty((0, 2, 128), dtype=torch.bfloat16, device="cuda:0")
     k = torch.zeros((40, 2, 128), dtype=torch.bfloat16, device="cuda:0")
