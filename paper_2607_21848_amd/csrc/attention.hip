@@ -401,8 +401,6 @@ __device__ __forceinline__ void wg_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// Scheduling-group masks of the interleave hints.
-constexpr int kSchedMfma = 0x008, kSchedValu = 0x002, kSchedDsRead = 0x100;
 
 template <bool kBias>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, BiasGeom g, float c_log2, KeySplit ks) {
@@ -689,6 +687,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         if constexpr (kind == 0) load_tile_lds(Kg, refill, (t0 + j + 3) * kTK, Lk, row_stride, tl, hd, wave, lane);
         if constexpr (kind <= 1) load_tile_lds(Vg, refill + kTileBytes, (t0 + j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
 
+        // K_{j+1} operands of the first QK MFMAs, read while the rescale check runs
+        const int nk0 = (t0 + j + 1) * kTK;
+        auto kread = [&](int kk) -> bf16x8 { return as_bf16x8(*reinterpret_cast<const u32x4*>(knext + koff[kk])); };
+        bf16x8 kf[8];
+        if constexpr (has_next) {
+            kf[0] = kread(0);
+            kf[1] = kread(1);
+            kf[2] = kread(2);
+        }
+
         // row maximum of tile j (reduced during the previous step) and lazy rescale
         const float mx = half_swap_max(mx_cur) * c_log2;
         if (__any(mx > m_run + kRescaleSlack)) {
@@ -700,64 +708,84 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             for (int db = 0; db < 4; ++db) O[db] *= alpha;
             m_run = m_new;
         }
-
-        // region A: QK of tile j + 1 on the matrix cores, probabilities of tile j on the VALU
-        const int nk0 = (t0 + j + 1) * kTK;
-        if constexpr (has_next) qk_tile(knext, nk0, S_next);
-        bf16x8 pf[2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            uint32_t w4[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(S_cur[8 * t + 2 * e], c_log2, -m_run));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(S_cur[8 * t + 2 * e + 1], c_log2, -m_run));
-                w4[e] = cvt_pk_bf16(p0, p1);
-                if (e & 1) {
-                    l_run1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
-                                                             __builtin_bit_cast(bf16x2, ones2), l_run1, false);
-                } else {
-                    l_run0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[e]),
-                                                             __builtin_bit_cast(bf16x2, ones2), l_run0, false);
-                }
-            }
-            pf[t] = as_bf16x8(u32x4{w4[0], w4[1], w4[2], w4[3]});
-        }
         if constexpr (has_next) {
-            // LDS reads run ahead of the MFMAs that consume them
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(kSchedValu, 6, 0);
-            }
+            if constexpr (kBias) S_next = bias_init(nk0);
+            else S_next = floatx16{0};
         }
 
-        // region B: PV of tile j on the matrix cores, row maximum of tile j + 1 on the VALU
-        float mx_next = -INFINITY;
-        if constexpr (has_next) mx_next = tile_max(std::integral_constant<bool, kind == 2>{}, S_next, nk0);
+        // The rest of the step is scheduled by hand: every chunk below ends in
+        // a scheduling fence, and pairs matrix-core work with VALU work that
+        // does not depend on it, so that one wave keeps both units busy.
+        // softmax unit (t, e): probabilities of logits 8 t + 2 e and 8 t + 2 e + 1
+        // of tile j, packed to bf16 and added to the running sums
+        uint32_t w4[2][4];
+        auto unit = [&](int t, int e) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(S_cur[8 * t + 2 * e], c_log2, -m_run));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(S_cur[8 * t + 2 * e + 1], c_log2, -m_run));
+            w4[t][e] = cvt_pk_bf16(p0, p1);
+            float& l = (e & 1) ? l_run1 : l_run0;
+            l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4[t][e]), __builtin_bit_cast(bf16x2, ones2),
+                                                l, false);
+        };
+        // V_j operand of the PV MFMA (key half t, head dims 32 db ..): two transposing reads
+        shortx4 vlo[2][4], vhi[2][4];
+        auto vread = [&](int t, int db) {
+            const uint8_t* vt = vcur + 16 * t * kRowBytes;
+            vlo[t][db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[0][db]));
+            vhi[t][db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[1][db]));
+        };
+        auto voperand = [&](int t, int db) -> bf16x8 {
+            const shortx4 lo = vlo[t][db], hi = vhi[t][db];
+            u32x4 w;
+            w[0] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[0], lo[1]});
+            w[1] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[2], lo[3]});
+            w[2] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[0], hi[1]});
+            w[3] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[2], hi[3]});
+            return as_bf16x8(w);
+        };
+        __builtin_amdgcn_sched_barrier(0);
+
+        // region A: the 8 QK MFMAs of tile j + 1 (K operands read three ahead),
+        // softmax units (0, 0..3) and (1, 0..1), V reads of key half 0
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-#pragma unroll
-            for (int db = 0; db < 4; ++db) {
-                const uint8_t* vt = vcur + 16 * t * kRowBytes;
-                const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[0][db]));
-                const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_shortx4*)(vt + voff[1][db]));
-                u32x4 w;
-                w[0] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[0], lo[1]});
-                w[1] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){lo[2], lo[3]});
-                w[2] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[0], hi[1]});
-                w[3] = __builtin_bit_cast(uint32_t, (short __attribute__((ext_vector_type(2)))){hi[2], hi[3]});
-                O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t], O[db], 0, 0, 0);
+        for (int kk = 0; kk < 8; ++kk) {
+            if constexpr (has_next) {
+                if (kk + 3 < 8) kf[kk + 3] = kread(kk + 3);
+                S_next = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], S_next, 0, 0, 0);
             }
+            if (kk < 6) unit(kk >> 2, kk & 3);
+            if (kk >= 4) vread(0, kk - 4);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 1);
+        const bf16x8 pf0 = as_bf16x8(u32x4{w4[0][0], w4[0][1], w4[0][2], w4[0][3]});
+
+        // region B1: PV of key half 0, softmax units (1, 2..3), V reads of key half 1
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 1);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 1);
-            __builtin_amdgcn_sched_group_barrier(kSchedValu, 1, 1);
+        for (int db = 0; db < 4; ++db) {
+            O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(voperand(0, db), pf0, O[db], 0, 0, 0);
+            if (db < 2) unit(1, 2 + db);
+            vread(1, db);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const bf16x8 pf1 = as_bf16x8(u32x4{w4[1][0], w4[1][1], w4[1][2], w4[1][3]});
+
+        // region B2: PV of key half 1, row maximum of tile j + 1 (keys past Lk
+        // masked when tile j + 1 is the last)
+        float mx_next = -INFINITY;
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+            O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(voperand(1, db), pf1, O[db], 0, 0, 0);
+            if constexpr (has_next) {
+#pragma unroll
+                for (int i = 4 * db; i < 4 * db + 4; ++i) {
+                    if constexpr (kind == 2) {
+                        if (nk0 + 16 * (i >> 3) + 8 * hh + (i & 7) >= Lk) S_next[i] = -INFINITY;
+                    }
+                }
+                if (db == 0) mx_next = max3(S_next[0], S_next[1], fmaxf(S_next[2], S_next[3]));
+                else mx_next = max3(mx_next, max3(S_next[4 * db], S_next[4 * db + 1], S_next[4 * db + 2]), S_next[4 * db + 3]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
         mx_cur = mx_next;
     };
