@@ -237,7 +237,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "attn_bf16_kernel",
+            "kernel": "attn_bf16_kernel (+ attn_merge_kernel when the keys are split)",
             "achieved": round(attn_tflops, 2),
             "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
