@@ -66,6 +66,7 @@ int retrieve_chunks(const float* bank_c2w, int32_t n_bank, const float* query_c2
                     int32_t first_candidate, int32_t k, int32_t* out_idx, float* out_score, int32_t* out_count,
                     int32_t frames_per_chunk, int32_t* out_frame_sel, hipStream_t stream) {
     if (n_bank < 0 || n_query < 0) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: negative n_bank or n_query");
+    if (n_bank > (1 << 30)) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: n_bank=%d above 2^30", n_bank);
     if (k < 1 || k > REVISIT_MAX_K) return fail(REVISIT_ERR_PARAM, "retrieve_chunks: k=%d outside [1, %d]", k, REVISIT_MAX_K);
     if (!(finite(E) && E > 0.0f)) return fail(REVISIT_ERR_PARAM, "retrieve_chunks: E must be finite and > 0");
     if (!finite(w_v) || !finite(tau_c) || !finite(tau_v))
@@ -75,6 +76,8 @@ int retrieve_chunks(const float* bank_c2w, int32_t n_bank, const float* query_c2
     if (n_query == 0) return REVISIT_OK;
     if (!query_c2w || !query_chunk || !out_idx || !out_count || (n_bank > 0 && !bank_c2w))
         return fail(REVISIT_ERR_NULL, "retrieve_chunks: required pointer is NULL");
+    // the scan reads the pose columns it needs as 8-byte pairs
+    if (!aligned(bank_c2w, 8)) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: bank_c2w must be 8-byte aligned");
     revisit::RetrieveArgs a;
     a.bank_c2w = bank_c2w;
     a.n_bank = n_bank;
@@ -93,6 +96,18 @@ int retrieve_chunks(const float* bank_c2w, int32_t n_bank, const float* query_c2
     a.out_count = out_count;
     a.frames_per_chunk = frames_per_chunk;
     a.out_frame_sel = out_frame_sel;
+    a.n_seg = revisit::retrieve_segments(n_bank);
+    a.seg_s = nullptr;
+    a.seg_j = nullptr;
+    if (a.n_seg > 0) {
+        if ((int64_t)a.n_seg * n_query * k > ((int64_t)1 << 31))
+            return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: n_bank * n_query too large");
+        void* ws = nullptr;
+        const hipError_t e = revisit::stream_workspace(stream, revisit::retrieve_workspace_bytes(n_bank, n_query, k), &ws);
+        if (e != hipSuccess) return fail(REVISIT_ERR_LAUNCH, "retrieve_chunks: workspace: %s", hipGetErrorString(e));
+        a.seg_s = static_cast<double*>(ws);
+        a.seg_j = reinterpret_cast<int32_t*>(a.seg_s + (size_t)a.n_seg * n_query * k);
+    }
     return launched(revisit::launch_retrieve(a, stream), "retrieve_chunks");
 }
 

@@ -34,7 +34,15 @@ struct RetrieveArgs {
     int32_t* out_count;
     int32_t frames_per_chunk;
     int32_t* out_frame_sel;
+    // segmented path for large banks (retrieve_segments(n_bank) > 0): per
+    // (query, segment) the k best (score, j), from a workspace of
+    // retrieve_workspace_bytes
+    int32_t n_seg;
+    double* seg_s;
+    int32_t* seg_j;
 };
+int32_t retrieve_segments(int32_t n_bank);
+size_t retrieve_workspace_bytes(int32_t n_bank, int32_t n_query, int32_t k);
 hipError_t launch_retrieve(const RetrieveArgs& a, hipStream_t stream);
 
 struct ReprojectArgs {

@@ -66,7 +66,8 @@ def _retrieve(L, **kw):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(k=0), 4), (dict(k=33), 4), (dict(E=0.0), 4), (dict(E=float("nan")), 4), (dict(tau_c=float("inf")), 4),
-    (dict(n_bank=-1), 2), (dict(n_query=-2), 2), (dict(query=NULL), 1), (dict(count=NULL), 1),
+    (dict(n_bank=-1), 2), (dict(n_bank=(1 << 30) + 1), 2), (dict(n_query=-2), 2), (dict(query=NULL), 1),
+    (dict(count=NULL), 1), (dict(bank=ctypes.c_void_p(0x1004)), 2),
     (dict(sel=FAKE, F=0), 4),
 ])
 def test_retrieve_rejects(L, kw, status):

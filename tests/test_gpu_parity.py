@@ -105,6 +105,43 @@ def test_retrieval_duplicates_tie_by_index():
     assert gc[0] == 8 and gi[0].tolist() == list(range(2, 10)) and (gsc[0] == 0).all()
 
 
+@pytest.mark.parametrize("N,k", [(8193, 4), (20000, 32), (100003, 4)])
+def test_retrieval_segmented_banks(N, k):
+    """Banks above 8192 entries take the segmented scan (one wave per 1024
+    entries, then a merge): same results as the oracle, bit for bit."""
+    from workloads.synth import ring_bank
+    rng = np.random.default_rng(N)
+    bank = ring_bank(rng, N, radius=6.0)
+    q = ring_bank(rng, 5, radius=6.0)
+    qchunk = np.array([N + 10, N // 2, 5, N - 1, 3 * N // 4], np.int32)
+    r = W.configs.Retrieval(bank_c2w=bank, query_c2w=q, query_chunk=qchunk, E=12.0, w_v=0.5, tau_c=0.1,
+                            tau_v=0.8, delta=3, first_candidate=1, k=k)
+    _check_retrieval(r)
+
+
+def test_retrieval_segmented_ties_cross_segments():
+    """Equal scores in every segment: the merge keeps the smallest indices."""
+    bank = np.tile(np.eye(4, dtype=np.float32), (20000, 1, 1))
+    r = W.configs.Retrieval(bank_c2w=bank, query_c2w=np.eye(4, dtype=np.float32)[None],
+                            query_chunk=np.array([30000], np.int32), E=1.0, w_v=0.5, tau_c=0.1, tau_v=0.5,
+                            delta=3, first_candidate=4000, k=32)
+    gi, gsc, gc, _ = _gpu_retrieve(r)
+    assert gc[0] == 32 and gi[0].tolist() == list(range(4000, 4032)) and (gsc[0] == 0).all()
+
+
+def test_retrieval_stress_bank_512mib():
+    """The 2^23-entry (512 MiB) stress bank of the retrieval bandwidth figure,
+    one query, top-4: identical to the oracle."""
+    from workloads.synth import ring_bank
+    rng = np.random.default_rng(23)
+    N = 1 << 23
+    bank = ring_bank(rng, N, radius=20.0)
+    q = ring_bank(rng, 1, radius=20.0)
+    r = W.configs.Retrieval(bank_c2w=bank, query_c2w=q, query_chunk=np.array([N + 5], np.int32), E=40.0,
+                            w_v=0.5, tau_c=0.05, tau_v=float(np.pi / 4), delta=3, first_candidate=1, k=4)
+    _check_retrieval(r)
+
+
 # --------------------------------------------------------------------------
 # reprojection
 # --------------------------------------------------------------------------

@@ -124,3 +124,25 @@ def noisy_plane_depth(rng, c2w, K, H, W, plane, z_lo, z_hi, noise_std) -> np.nda
     t = render_planes(c2w, K, H, W, [plane], z_lo, z_hi)
     t = t + rng.normal(0.0, noise_std, size=t.shape)
     return np.clip(t, z_lo, z_hi)
+
+
+def ring_bank(rng: np.random.Generator, n: int, radius: float, height: float = 1.5,
+              yaw_jitter_deg: float = 10.0) -> np.ndarray:
+    """n camera-to-world poses [n, 4, 4] fp32 scattered over a disc of the
+    given radius at a fixed height (world z up), each looking horizontally
+    along the tangent of its circle plus a uniform yaw jitter: look_pose with
+    pitch 0, vectorised for large stress banks."""
+    rad = radius * np.sqrt(rng.uniform(0.0, 1.0, n))
+    phi = rng.uniform(0.0, 2.0 * np.pi, n)
+    yaw = phi + 0.5 * np.pi + np.deg2rad(rng.uniform(-yaw_jitter_deg, yaw_jitter_deg, n))
+    c, s = np.cos(yaw), np.sin(yaw)
+    out = np.zeros((n, 4, 4), np.float32)
+    # columns: right = forward x up = (s, -c, 0), down = (0, 0, -1), forward = (c, s, 0)
+    out[:, 0, 0], out[:, 1, 0] = s, -c
+    out[:, 2, 1] = -1.0
+    out[:, 0, 2], out[:, 1, 2] = c, s
+    out[:, 0, 3] = rad * np.cos(phi)
+    out[:, 1, 3] = rad * np.sin(phi)
+    out[:, 2, 3] = height
+    out[:, 3, 3] = 1.0
+    return out
