@@ -11,7 +11,7 @@
 // source depth around u^ (cache-resident: a source frame is at most a few
 // hundred KB) and the visibility test. Outputs are structure-of-arrays
 // [B][S][Tq*h*w] so that for every s consecutive threads store consecutive
-// tokens (8-byte u^ pairs and 4-byte codes, fully coalesced).
+// tokens (u^ pairs and codes, fully coalesced, non-temporal).
 //
 // Arithmetic is IEEE double in the order of the definition with
 // contraction disabled; the code and u^ (rounded to fp32 once) are
@@ -65,6 +65,79 @@ __device__ __forceinline__ double per_token(float k, double pd) {
     else return (double)k / pd;
 }
 
+// Outputs are written once and never read back by this kernel: non-temporal
+// stores keep them from displacing the depth maps in the caches.
+__device__ __forceinline__ void st_uv(float2* p, float2 v) {
+    __builtin_nontemporal_store(v.x, &p->x);
+    __builtin_nontemporal_store(v.y, &p->y);
+}
+__device__ __forceinline__ void st_code(int32_t* p, int v) { __builtin_nontemporal_store(v, p); }
+
+// A target token lifted to the world: R_t X_t + c_t, or undefined depth.
+struct Lifted {
+    double W[3];
+    bool defined;
+};
+
+// Result for one (token, source): u^ (NaN when not computed) and the code.
+struct Corr {
+    float2 uv;
+    int code;
+};
+
+// Source frame s of the block's problem, converted to doubles in LDS:
+// R (row-major), c, token-grid (fx, fy, cx, cy); frame index -1 = no source.
+struct SrcFrames {
+    double c[kMaxSrcLds][16];
+    int f[kMaxSrcLds];
+};
+
+template <int P>
+__device__ __forceinline__ Lifted lift(double z, int i, int j, double fxt, double fyt, double cxt, double cyt,
+                                       const float* Mt) {
+    Lifted L;
+    L.defined = isfinite(z) && z > 0.0;
+    // X_t = z K_t^-1 u~, then R_t X_t + c_t (the source centre comes later)
+    const double ux = (double)j + 0.5, uy = (double)i + 0.5;
+    const double Xt = ((ux - cxt) / fxt) * z;
+    const double Yt = ((uy - cyt) / fyt) * z;
+    const double Zt = z;
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+        L.W[r] = (((double)Mt[4 * r + 0] * Xt + (double)Mt[4 * r + 1] * Yt) + (double)Mt[4 * r + 2] * Zt) +
+                 (double)Mt[4 * r + 3];
+    }
+    return L;
+}
+
+// Eq. reprojection and Eq. visibility for one (lifted token, source frame s).
+template <int P>
+__device__ __forceinline__ Corr correspond(const ReprojectArgs& a, const Lifted& L, const SrcFrames& sf, int s, int Wd,
+                                           size_t frame_px, int p, double tol) {
+    const int f = sf.f[s];
+    if (f < 0) return Corr{make_float2(NAN, NAN), -5};
+    if (!L.defined) return Corr{make_float2(NAN, NAN), -1};
+    const double* C = sf.c[s];
+    // R_t X_t + c_t - c_s
+    const double W0 = L.W[0] - C[9];
+    const double W1 = L.W[1] - C[10];
+    const double W2 = L.W[2] - C[11];
+    // X_s = R_s^T (...): component r is column r of R_s dotted with W
+    const double Xs = (C[0] * W0 + C[3] * W1) + C[6] * W2;
+    const double Ys = (C[1] * W0 + C[4] * W1) + C[7] * W2;
+    const double Zs = (C[2] * W0 + C[5] * W1) + C[8] * W2;
+    if (!(Zs > 0.0)) return Corr{make_float2(NAN, NAN), -2};
+    const double fxs = C[12], fys = C[13], cxs = C[14], cys = C[15];
+    const double uhx = (fxs * Xs + cxs * Zs) / Zs;
+    const double uhy = (fys * Ys + cys * Zs) / Zs;
+    const float2 uv = make_float2((float)uhx, (float)uhy);
+    if (!(uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h)) return Corr{uv, -3};
+    const int kx = (int)floor(uhx);
+    const int ky = (int)floor(uhy);
+    const double Ds = pooled<P>(a.src_depth + (size_t)f * frame_px, Wd, ky, kx, p);
+    return Corr{uv, (Zs <= tol * Ds) ? ky * a.w + kx : -4};
+}
+
 template <int P>
 __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const int hw = a.h * a.w;
@@ -92,43 +165,26 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const float* Kt = a.tgt_K + (size_t)bt * 4;
     const double fxt = per_token<P>(Kt[0], pd), fyt = per_token<P>(Kt[1], pd);
     const double cxt = per_token<P>(Kt[2], pd), cyt = per_token<P>(Kt[3], pd);
-
-    const double z = pooled<P>(a.tgt_depth + (size_t)bt * frame_px, Wd, i, j, p);
-    const bool defined = isfinite(z) && z > 0.0;
-
-    // X_t = z K_t^-1 u~, then R_t X_t + c_t (the source centre comes later)
-    const double ux = (double)j + 0.5, uy = (double)i + 0.5;
-    const double Xt = ((ux - cxt) / fxt) * z;
-    const double Yt = ((uy - cyt) / fyt) * z;
-    const double Zt = z;
-    double Wt[3];
-#pragma unroll
-    for (int r = 0; r < 3; ++r) {
-        Wt[r] = (((double)Mt[4 * r + 0] * Xt + (double)Mt[4 * r + 1] * Yt) + (double)Mt[4 * r + 2] * Zt) +
-                (double)Mt[4 * r + 3];
-    }
+    const Lifted L = lift<P>(pooled<P>(a.tgt_depth + (size_t)bt * frame_px, Wd, i, j, p), i, j, fxt, fyt, cxt, cyt, Mt);
     const double tol = 1.0 + a.eps;
 
-    // Source frames of this problem, converted once per block into LDS as
-    // doubles: R (row-major), c, token-grid (fx, fy, cx, cy); frame index -1 =
-    // no source. The loop below then reads them as broadcasts.
-    __shared__ double src_c[kMaxSrcLds][16];
-    __shared__ int src_f[kMaxSrcLds];
+    // the problem's source frames, converted once per block
+    __shared__ SrcFrames sf;
     for (int s = threadIdx.x; s < a.S; s += kBlock) {
         int f = b * a.S + s;
         if (a.src_sel) {
             f = a.src_sel[(size_t)b * a.S + s];
             if (f < 0 || f >= a.n_src) f = -1;
         }
-        src_f[s] = f;
+        sf.f[s] = f;
         if (f >= 0) {
             const float* Ms = a.src_c2w + (size_t)f * 16;
             const float* Ks = a.src_K + (size_t)f * 4;
             for (int r = 0; r < 3; ++r) {
-                for (int c = 0; c < 3; ++c) src_c[s][3 * r + c] = (double)Ms[4 * r + c];
-                src_c[s][9 + r] = (double)Ms[4 * r + 3];
+                for (int c = 0; c < 3; ++c) sf.c[s][3 * r + c] = (double)Ms[4 * r + c];
+                sf.c[s][9 + r] = (double)Ms[4 * r + 3];
             }
-            for (int c = 0; c < 4; ++c) src_c[s][12 + c] = per_token<P>(Ks[c], pd);
+            for (int c = 0; c < 4; ++c) sf.c[s][12 + c] = per_token<P>(Ks[c], pd);
         }
     }
     __syncthreads();
@@ -136,44 +192,9 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
 
     for (int s = 0; s < a.S; ++s) {
         const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
-        float2* uv_out = reinterpret_cast<float2*>(a.out_uv) + o;
-        const int f = src_f[s];
-        if (f < 0) {
-            *uv_out = make_float2(NAN, NAN);
-            a.out_idx[o] = -5;
-            continue;
-        }
-        if (!defined) {
-            *uv_out = make_float2(NAN, NAN);
-            a.out_idx[o] = -1;
-            continue;
-        }
-        const double* C = src_c[s];
-        // R_t X_t + c_t - c_s
-        const double W0 = Wt[0] - C[9];
-        const double W1 = Wt[1] - C[10];
-        const double W2 = Wt[2] - C[11];
-        // X_s = R_s^T (...): component r is column r of R_s dotted with W
-        const double Xs = (C[0] * W0 + C[3] * W1) + C[6] * W2;
-        const double Ys = (C[1] * W0 + C[4] * W1) + C[7] * W2;
-        const double Zs = (C[2] * W0 + C[5] * W1) + C[8] * W2;
-        if (!(Zs > 0.0)) {
-            *uv_out = make_float2(NAN, NAN);
-            a.out_idx[o] = -2;
-            continue;
-        }
-        const double fxs = C[12], fys = C[13], cxs = C[14], cys = C[15];
-        const double uhx = (fxs * Xs + cxs * Zs) / Zs;
-        const double uhy = (fys * Ys + cys * Zs) / Zs;
-        *uv_out = make_float2((float)uhx, (float)uhy);
-        if (!(uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h)) {
-            a.out_idx[o] = -3;
-            continue;
-        }
-        const int kx = (int)floor(uhx);
-        const int ky = (int)floor(uhy);
-        const double Ds = pooled<P>(a.src_depth + (size_t)f * frame_px, Wd, ky, kx, p);
-        a.out_idx[o] = (Zs <= tol * Ds) ? ky * a.w + kx : -4;
+        const Corr c = correspond<P>(a, L, sf, s, Wd, frame_px, p, tol);
+        st_uv(reinterpret_cast<float2*>(a.out_uv) + o, c.uv);
+        st_code(a.out_idx + o, c.code);
     }
 }
 
