@@ -224,12 +224,18 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
 // Pipeline. K runs one tile ahead of V: in step j a wave computes
 // S_{j+1} = K_{j+1} Q^T on the matrix cores while its VALU turns S_j into
 // probabilities, then accumulates O += P_j V_j while the VALU reduces the
-// row maxima of S_{j+1}. Instruction groups are interleaved explicitly
-// (MFMA / LDS / VALU), so the exponentials hide behind the matrix work of
-// the same wave, and the second wave of the SIMD fills remaining gaps. Two
-// K and two V buffers; the loads for tiles j+2 (K) and j+1 (V) are issued
-// right after the one barrier of step j. Workgroups are mapped XCD-aware
-// (head-major) so the workgroups of one head share an L2.
+// row maxima of S_{j+1}. The LDS holds a ring of three slots; slot t mod 3
+// carries K_t and V_{t-1}. Right after its one barrier, step j refills slot
+// j mod 3 (no wave reads K_j or V_{j-1} any more) with K_{j+3} and V_{j+2},
+// so a direct load has two steps to land and each lane waits only for its
+// loads of two steps back. The steady loop is unrolled over a period of six
+// (ring slot and current logit registers are then compile-time). Inside a
+// step the instruction order is fixed by hand with scheduling fences: each
+// QK MFMA carries one softmax unit and the K reads three MFMAs ahead, the
+// PV MFMAs carry the V transpose reads and the row maxima, so one wave keeps
+// the matrix cores and the VALU busy and the second wave of the SIMD fills
+// the gaps. Work units are mapped XCD-aware so the workgroups of one head
+// (and key range) share an L2.
 //
 // Softmax. exp2 on the raw hardware instruction with scale * log2(e) folded
 // into one FMA, probabilities packed to bf16 pairwise and summed with bf16
