@@ -17,11 +17,15 @@ Modules, each citing the passage of the paper it writes out:
 * ``attention``    -- scaled dot-product attention with the Gaussian
   correspondence bias on retrieved-frame key columns (Sec. 4.3, Eq. bias,
   design choices (ii) and (iii));
-* ``brute``        -- pure-Python loop versions of the three, for tiny
+* ``kvpack``       -- reinstating retrieved chunks into the cache: gather
+  of their keys and values and re-rotation of the keys' temporal position
+  embedding to the packed positions (Sec. 4.2, cache layout and cache
+  packing);
+* ``brute``        -- pure-Python loop versions of the first three, for tiny
   inputs, used to pin the vectorised ones.
 
 Every function here has pins in ``tests/test_oracle_*.py`` (closed forms,
 invariants, library reductions, brute force); none is "parity unpinned".
 """
 
-from . import attention, brute, reprojection, retrieval  # noqa: F401
+from . import attention, brute, kvpack, reprojection, retrieval  # noqa: F401
