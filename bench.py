@@ -12,7 +12,10 @@ the whole step (4 Lq Lk D H flops per step / step time). ``roofline``
 describes the dominant kernel (biased attention) from HIP events recorded on
 its launch stream; ``stages`` adds per-stage times, the reprojection
 throughput of a batched launch (1024 independent problems, > 2x the 256 MB
-last-level cache) and retrieval latency; ``cpu_baseline`` times the fp64
+last-level cache), retrieval latency, the retrieval bandwidth on a stress
+bank, and the cache packing of the step's retrieved chunks for all 30
+layers from a store of every bank chunk's keys and values (HBM-bound, not
+part of the step); ``cpu_baseline`` times the fp64
 oracle on a bounded sample of the same workload on this host.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
@@ -38,11 +41,13 @@ METRIC = "biased-attention TFLOP/s + MFMA util; reprojection tokens/s (Wan-1.3B 
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 BENCH_QUERY = 1  # query chunk n = 225: a full top-4 retrieval
+PACK_LAYERS = 30  # transformer blocks of the 1.3B backbone: one packing call covers all of them
+ROPE_T_PAIRS, ROPE_THETA = 22, 10000.0  # temporal band of the factorised 3-D RoPE at head dim 128
 REPROJ_BATCH = 1024
 
 
 def profiled_counters():
-    """HBM traffic of the attention / reprojection kernels as last measured with
+    """HBM traffic of the attention / reprojection / packing kernels as last measured with
     rocprofv3 (profiles/counters.json), valid only while the kernel sources are
     unchanged since the counters were taken."""
     import hashlib
@@ -53,7 +58,7 @@ def profiled_counters():
         c = json.load(f)
     src = os.path.join(ROOT, "paper_2607_21848_amd", "csrc")
     out = {}
-    for key, fname in (("attention", "attention.hip"), ("reproject", "reproject.hip")):
+    for key, fname in (("attention", "attention.hip"), ("reproject", "reproject.hip"), ("kvpack", "kvpack.hip")):
         with open(os.path.join(src, fname), "rb") as f:
             sha = hashlib.sha256(f.read()).hexdigest()[:16]
         if c.get(f"{key}_sha") == sha:
@@ -238,6 +243,42 @@ def main():
     log(f"retrieval stress {rs_ms * 1e3:.1f} us: {rs_gbs:.0f} GB/s algorithmic (64 B per pose)")
     del sbank, squery, schunk, sout
 
+    # cache packing: the query chunk's retrieved chunks (out_idx of the timed retrieval, on the device)
+    # gathered from a history store holding every bank chunk's keys and values for every layer, keys
+    # re-rotated to the packed frame positions 3..14 (after the anchor, ending where the recent window begins)
+    F_pack, T_pack = 3, 3 * wl.h * wl.w
+    pack_layer_bytes = 2 * (int(r.bank_c2w.shape[0]) * T_pack + wl.Lk) * wl.H * wl.D * 2
+    free_b = torch.cuda.mem_get_info(dev)[0]
+    pack_layers = int(max(1, min(PACK_LAYERS, (free_b - (24 << 30)) // pack_layer_bytes)))
+    log(f"cache packing: {pack_layers} layers x {r.k} chunks from a {int(r.bank_c2w.shape[0])}-chunk store "
+        f"({pack_layers * pack_layer_bytes / 1e9:.1f} GB allocated)")
+    n_bank = int(r.bank_c2w.shape[0])
+    store_k = torch.empty((pack_layers, n_bank, T_pack, wl.H, wl.D), dtype=torch.bfloat16, device=dev)
+    store_v = torch.empty_like(store_k)
+    cache_k = torch.zeros((pack_layers, wl.Lk, wl.H, wl.D), dtype=torch.bfloat16, device=dev)
+    cache_v = torch.zeros_like(cache_k)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(31)
+    psel = ridx[0]
+    for j in psel.tolist():  # only the selected chunks are ever read
+        store_k[:, j].normal_(generator=gen)
+        store_v[:, j].normal_(generator=gen)
+    pargs = dict(F=F_pack, h=wl.h, w=wl.w, dst_pos=F_pack, dst_row0=T_pack, rope_t_pairs=ROPE_T_PAIRS,
+                 rope_theta=ROPE_THETA)
+    for _ in range(3):
+        rv.pack_retrieved_kv(store_k, store_v, psel, cache_k, cache_v, **pargs)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        rv.pack_retrieved_kv(store_k, store_v, psel, cache_k, cache_v, **pargs)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    pk_ms = e0.elapsed_time(e1) / reps
+    pk_bytes = 2 * pack_layers * r.k * 2 * T_pack * wl.H * wl.D * 2  # K and V, read once and written once
+    pk_gbs = pk_bytes / (pk_ms * 1e-3) / 1e9
+    log(f"cache packing {pk_ms:.3f} ms: {pk_gbs:.0f} GB/s algorithmic")
+    del store_k, store_v, cache_k, cache_v
+
     counters = profiled_counters()
     out = {
         "metric": METRIC,
@@ -283,6 +324,12 @@ def main():
                 "achieved_GBs": round(rb_gbs, 1), "peak_GBs": HBM_PEAK_GBS,
                 "frac": round(rb_gbs / HBM_PEAK_GBS, 4), "bound": "hbm",
                 "traffic": counters.get("reproject"),
+            },
+            "kv_pack": {
+                "layers": pack_layers, "chunks": r.k, "tokens_per_chunk": T_pack, "store_chunks": n_bank,
+                "rope_t_pairs": ROPE_T_PAIRS, "ms": round(pk_ms, 4), "bytes": pk_bytes,
+                "achieved_GBs": round(pk_gbs, 1), "peak_GBs": HBM_PEAK_GBS, "frac": round(pk_gbs / HBM_PEAK_GBS, 4),
+                "bound": "hbm", "traffic": counters.get("kvpack"),
             },
             "retrieval_stress": {
                 "note": "stress bank outside the configs", "bank_poses": n_stress, "queries": 1, "top_k": 4,

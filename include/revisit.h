@@ -4,7 +4,8 @@
  * (arXiv 2607.21848: pose-retrieved loop-closure memory, Sec. 4.2, and the
  * geometric correspondence attention prior, Sec. 4.3).
  *
- * Three stages, one entry point each:
+ * Three stages, one entry point each, and the cache packing that puts the
+ * retrieved chunks in front of the attention:
  *
  *   retrieve_chunks           -- pose retrieval over the history bank
  *                                (Sec. 4.2, Eq. retrieval)
@@ -14,6 +15,9 @@
  *   biased_chunk_attention    -- chunk attention with the Gaussian
  *                                correspondence bias fused in
  *                                (Sec. 4.3, Eq. bias)
+ *   pack_retrieved_kv         -- gather of the retrieved chunks' keys and
+ *                                values into the cache, keys re-rotated to
+ *                                the packed positions (Sec. 4.2)
  *
  * Conventions common to all entry points
  * --------------------------------------
@@ -213,6 +217,55 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
                            const float* corr_uv, const int32_t* corr_idx, int32_t S,
                            float softmax_scale, float lambda, float sigma,
                            hipStream_t stream);
+
+/*
+ * pack_retrieved_kv -- Sec. 4.2, cache layout and cache packing.
+ *
+ * Reinstates retrieved chunks into the attention cache. The history store
+ * keeps every historical chunk's keys and values as the cache held them, keys
+ * carrying the rotary position embedding of temporal position pos[j] + f in
+ * frame f of chunk j. For every layer l and slot s with j = sel[s] in
+ * [0, n_store), and T = F h w tokens per chunk:
+ *     V_cache[l][dst_row0 + s T + r] = V_store[l][j][r]
+ *     K_cache[l][dst_row0 + s T + r] = K_store[l][j][r] with each temporal
+ *         pair (k_{2i}, k_{2i+1}), i < rope_t_pairs, read as k_{2i} + i k_{2i+1}
+ *         and multiplied by exp(i delta omega_i),
+ *         omega_i = rope_theta^(-i / rope_t_pairs),
+ *         delta = dst_pos + s F - pos[j]
+ * so slot s sits at frame positions dst_pos + s F .. dst_pos + s F + F - 1;
+ * the caller chooses dst_pos so that the slots end where the recent window
+ * begins (the paper places the retrieved chunk directly next to it). Pairs
+ * i >= rope_t_pairs (the grid row and column bands of the embedding) and all
+ * values are copied bit for bit. The rotation is evaluated in double
+ * precision (x c - y s, x s + y c) and rounded once to the storage type,
+ * to nearest even.
+ *
+ *   dtype         REVISIT_BF16 or REVISIT_F32; D a multiple of 8 in [8, 512]
+ *   store_k, store_v  [n_layers][n_store][T][H][D]   (chunk j at index j)
+ *   store_pos     nullable [n_store] int32: stored frame position of frame 0 of
+ *                 chunk j; NULL means F j (the chunk's original index)
+ *   sel           [n_sel] int32: chunk of each slot (e.g. out_idx of
+ *                 retrieve_chunks for one query); an entry outside
+ *                 [0, n_store) leaves that slot of the cache untouched (the
+ *                 caller fills it, e.g. with the recent-window extension
+ *                 when no chunk was admissible)
+ *   cache_k, cache_v  [n_layers][cache_rows][H][D]; the slots occupy rows
+ *                 [dst_row0, dst_row0 + n_sel T), which must fit in cache_rows
+ *   rope_t_pairs  temporal pairs, 0..D/2 (0 = plain gather); rope_theta > 0
+ *
+ * Store and cache must not overlap. store_k, store_v, cache_k, cache_v must be
+ * 16-byte aligned, sel and store_pos 4-byte aligned (REVISIT_ERR_SHAPE
+ * otherwise). n_layers == 0 or n_sel == 0 is valid (nothing to do); with
+ * n_store == 0 every slot is left untouched and the store pointers may be NULL.
+ */
+int pack_retrieved_kv(const void* store_k, const void* store_v,
+                      const int32_t* store_pos, int32_t n_store,
+                      const int32_t* sel, int32_t n_sel, int32_t dst_pos,
+                      void* cache_k, void* cache_v, int32_t dst_row0, int32_t cache_rows,
+                      int32_t n_layers, int32_t dtype,
+                      int32_t F, int32_t h, int32_t w, int32_t H, int32_t D,
+                      int32_t rope_t_pairs, float rope_theta,
+                      hipStream_t stream);
 
 /*
  * rc_set_attention_key_parts -- tuning knob of the bf16 attention work split

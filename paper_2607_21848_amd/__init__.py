@@ -25,7 +25,8 @@ import torch
 from . import _lib
 from ._lib import BF16, F32, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
 
-__all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "set_attention_key_parts",
+__all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "pack_retrieved_kv",
+           "set_attention_key_parts",
            "RevisitError", "lib"]
 
 
@@ -173,6 +174,43 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
                                       softmax_scale, lam, sigma, _stream(dev))
     _lib.check("biased_chunk_attention", st)
     return o, lse
+
+
+def pack_retrieved_kv(store_k: torch.Tensor, store_v: torch.Tensor, sel: torch.Tensor,
+                      cache_k: torch.Tensor, cache_v: torch.Tensor, *, F: int, h: int, w: int,
+                      dst_pos: int, dst_row0: int, rope_t_pairs: int, rope_theta: float,
+                      store_pos: Optional[torch.Tensor] = None) -> None:
+    """Copy the selected chunks' keys and values into the cache slots, in place.
+
+    store_k, store_v [L, n_store, F*h*w, H, D]; cache_k, cache_v [L, rows, H, D]
+    (bf16 or fp32, D a multiple of 8); sel [n_sel] i32 (entries outside
+    [0, n_store) leave their slot untouched); store_pos None or [n_store] i32.
+    Slot s goes to cache rows dst_row0 + s*F*h*w and frame position
+    dst_pos + s*F; the first rope_t_pairs pairs of each key are re-rotated."""
+    dev = cache_k.device
+    if store_k.dim() != 5 or cache_k.dim() != 4:
+        raise ValueError("store_k must be [L, n_store, T, H, D] and cache_k [L, rows, H, D]")
+    L, n_store, T, H, D = store_k.shape
+    rows = cache_k.shape[1]
+    if cache_k.dtype == torch.bfloat16:
+        dt = BF16
+    elif cache_k.dtype == torch.float32:
+        dt = F32
+    else:
+        raise TypeError(f"cache_k must be bfloat16 or float32 (got {cache_k.dtype})")
+    if T != F * h * w:
+        raise ValueError(f"store rows per chunk {T} != F*h*w = {F * h * w}")
+    _need(store_k, "store_k", cache_k.dtype, (L, n_store, T, H, D), dev)
+    _need(store_v, "store_v", cache_k.dtype, (L, n_store, T, H, D), dev)
+    _need(cache_k, "cache_k", cache_k.dtype, (L, rows, H, D), dev)
+    _need(cache_v, "cache_v", cache_k.dtype, (L, rows, H, D), dev)
+    _need(sel, "sel", torch.int32, None, dev)
+    if store_pos is not None:
+        _need(store_pos, "store_pos", torch.int32, (n_store,), dev)
+    st = lib().pack_retrieved_kv(_ptr(store_k), _ptr(store_v), _ptr(store_pos), n_store, _ptr(sel), sel.numel(),
+                                 int(dst_pos), _ptr(cache_k), _ptr(cache_v), int(dst_row0), rows, L, dt, F, h, w, H,
+                                 D, int(rope_t_pairs), float(rope_theta), _stream(dev))
+    _lib.check("pack_retrieved_kv", st)
 
 
 def set_attention_key_parts(parts: int) -> None:

@@ -17,7 +17,7 @@ OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH = 0, 1, 2, 3, 4,
 BF16, F32 = 1, 2
 MAX_K = 32
 EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
-            "biased_chunk_attention", "rc_set_attention_key_parts")
+            "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv")
 
 _p = ctypes.c_void_p
 _i = ctypes.c_int32
@@ -50,6 +50,9 @@ def lib() -> ctypes.CDLL:
         L.biased_chunk_attention.restype = ctypes.c_int
         L.biased_chunk_attention.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _i,
                                              _f, _f, _f, _p]
+        L.pack_retrieved_kv.restype = ctypes.c_int
+        L.pack_retrieved_kv.argtypes = [_p, _p, _p, _i, _p, _i, _i, _p, _p, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
+                                        _f, _p]
         L.rc_set_attention_key_parts.restype = ctypes.c_int
         L.rc_set_attention_key_parts.argtypes = [_i]
         _LIB = L

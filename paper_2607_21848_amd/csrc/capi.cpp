@@ -224,6 +224,60 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     return launched(revisit::launch_attention_bf16(a, parts, static_cast<float*>(ws), stream), "biased_chunk_attention");
 }
 
+int pack_retrieved_kv(const void* store_k, const void* store_v, const int32_t* store_pos, int32_t n_store,
+                      const int32_t* sel, int32_t n_sel, int32_t dst_pos, void* cache_k, void* cache_v,
+                      int32_t dst_row0, int32_t cache_rows, int32_t n_layers, int32_t dtype, int32_t F, int32_t h,
+                      int32_t w, int32_t H, int32_t D, int32_t rope_t_pairs, float rope_theta, hipStream_t stream) {
+    if (dtype != REVISIT_BF16 && dtype != REVISIT_F32)
+        return fail(REVISIT_ERR_UNSUPPORTED, "pack_retrieved_kv: dtype %d not supported", dtype);
+    if (D < 8 || D > 512 || D % 8 != 0)
+        return fail(REVISIT_ERR_UNSUPPORTED, "pack_retrieved_kv: D=%d (need a multiple of 8 in [8, 512])", D);
+    if (n_store < 0 || n_sel < 0 || n_layers < 0 || F < 1 || h < 1 || w < 1 || H < 1 || dst_row0 < 0 || cache_rows < 0)
+        return fail(REVISIT_ERR_SHAPE, "pack_retrieved_kv: need n_store, n_sel, n_layers, dst_row0, cache_rows >= 0 "
+                                       "and F, h, w, H >= 1");
+    const int64_t T = (int64_t)F * h * w;
+    if (T > INT32_MAX) return fail(REVISIT_ERR_SHAPE, "pack_retrieved_kv: F*h*w too large");
+    if ((int64_t)dst_row0 + (int64_t)n_sel * T > cache_rows)
+        return fail(REVISIT_ERR_SHAPE, "pack_retrieved_kv: %d slots of %lld rows from row %d exceed cache_rows=%d", n_sel,
+                    (long long)T, dst_row0, cache_rows);
+    const int64_t row = (int64_t)H * D;
+    if ((double)n_layers * n_store * T * row > (double)kMaxElems || (double)n_layers * cache_rows * row > (double)kMaxElems)
+        return fail(REVISIT_ERR_SHAPE, "pack_retrieved_kv: store or cache too large");
+    if (rope_t_pairs < 0 || rope_t_pairs > D / 2)
+        return fail(REVISIT_ERR_PARAM, "pack_retrieved_kv: rope_t_pairs=%d outside [0, D/2]", rope_t_pairs);
+    if (rope_t_pairs > 0 && !(finite(rope_theta) && rope_theta > 0.0f))
+        return fail(REVISIT_ERR_PARAM, "pack_retrieved_kv: rope_theta must be finite and > 0");
+    if (n_layers == 0 || n_sel == 0) return REVISIT_OK;
+    if (!sel || !cache_k || !cache_v || (n_store > 0 && (!store_k || !store_v)))
+        return fail(REVISIT_ERR_NULL, "pack_retrieved_kv: required pointer is NULL");
+    // the kernel moves 16-byte vectors
+    if (!aligned(store_k, 16) || !aligned(store_v, 16) || !aligned(cache_k, 16) || !aligned(cache_v, 16) ||
+        !aligned(sel, 4) || !aligned(store_pos, 4))
+        return fail(REVISIT_ERR_SHAPE, "pack_retrieved_kv: store and cache must be 16-byte aligned, sel and store_pos 4-byte");
+    revisit::KvPackArgs a;
+    a.store_k = store_k;
+    a.store_v = store_v;
+    a.store_pos = store_pos;
+    a.n_store = n_store;
+    a.sel = sel;
+    a.n_sel = n_sel;
+    a.dst_pos = dst_pos;
+    a.cache_k = cache_k;
+    a.cache_v = cache_v;
+    a.dst_row0 = dst_row0;
+    a.cache_rows = cache_rows;
+    a.n_layers = n_layers;
+    a.esize = dtype == REVISIT_BF16 ? 2 : 4;
+    a.F = F;
+    a.T = (int32_t)T;
+    a.H = H;
+    a.D = D;
+    a.n_t = rope_t_pairs;
+    a.theta = (double)rope_theta;
+    if (revisit::kvpack_blocks(a) > INT32_MAX) return fail(REVISIT_ERR_SHAPE, "pack_retrieved_kv: problem too large");
+    return launched(revisit::launch_kvpack(a, stream), "pack_retrieved_kv");
+}
+
 int rc_set_attention_key_parts(int32_t parts) {
     if (parts < 0 || parts > kMaxKeyParts)
         return fail(REVISIT_ERR_PARAM, "rc_set_attention_key_parts: %d outside [0, %d]", parts, kMaxKeyParts);

@@ -87,6 +87,33 @@ hipError_t launch_attention_bf16(const AttentionArgs& a, int32_t parts, float* w
 
 // Library-owned device memory of `bytes` for work queued on `stream` of the
 // current device (see workspace.cpp); compute units of the current device.
+// Cache packing of retrieved chunks (kvpack.hip). Element size 2 (bf16) or
+// 4 (fp32); T = tokens per chunk; store [L][n_store][T][H][D], cache
+// [L][cache_rows][H][D].
+struct KvPackArgs {
+    const void* store_k;
+    const void* store_v;
+    const int32_t* store_pos;  // nullable: chunk j at frame position F j
+    int32_t n_store;
+    const int32_t* sel;
+    int32_t n_sel;
+    int32_t dst_pos;
+    void* cache_k;
+    void* cache_v;
+    int32_t dst_row0;
+    int32_t cache_rows;
+    int32_t n_layers;
+    int32_t esize;
+    int32_t F;
+    int32_t T;
+    int32_t H;
+    int32_t D;
+    int32_t n_t;
+    double theta;
+};
+int64_t kvpack_blocks(const KvPackArgs& a);
+hipError_t launch_kvpack(const KvPackArgs& a, hipStream_t stream);
+
 hipError_t stream_workspace(hipStream_t stream, size_t bytes, void** out);
 hipError_t device_compute_units(int* cus);
 

@@ -29,8 +29,8 @@ def declared_functions():
 
 def test_header_declares_the_three_stages():
     names = declared_functions()
-    for n in ("retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "rc_status_string",
-              "rc_last_error", "rc_set_attention_key_parts"):
+    for n in ("retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "pack_retrieved_kv",
+              "rc_status_string", "rc_last_error", "rc_set_attention_key_parts"):
         assert n in names
 
 
@@ -132,3 +132,33 @@ def test_attention_bias_pointers_optional_when_off(L):
 def test_attention_key_parts_knob(L, n, status):
     assert L.rc_set_attention_key_parts(n) == status
     L.rc_set_attention_key_parts(0)
+
+
+def _pack(L, **kw):
+    a = dict(sk=FAKE, sv=FAKE, pos=NULL, n_store=200, sel=FAKE, n_sel=4, dst_pos=3, ck=FAKE, cv=FAKE, row0=4680,
+             rows=37440, layers=30, dtype=1, F=3, h=30, w=52, H=12, D=128, nt=22, theta=10000.0)
+    a.update(kw)
+    return L.pack_retrieved_kv(a["sk"], a["sv"], a["pos"], a["n_store"], a["sel"], a["n_sel"], a["dst_pos"], a["ck"],
+                               a["cv"], a["row0"], a["rows"], a["layers"], a["dtype"], a["F"], a["h"], a["w"], a["H"],
+                               a["D"], a["nt"], a["theta"], NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=3), 3), (dict(D=60), 3), (dict(D=0), 3), (dict(D=520), 3),
+    (dict(F=0), 2), (dict(H=0), 2), (dict(n_store=-1), 2), (dict(n_sel=-1), 2), (dict(layers=-1), 2), (dict(row0=-1), 2),
+    (dict(row0=18721), 2), (dict(n_sel=8), 2), (dict(rows=1 << 30, layers=1 << 14), 2),
+    (dict(nt=-1), 4), (dict(nt=65), 4), (dict(theta=0.0), 4), (dict(theta=float("nan")), 4),
+    (dict(sk=NULL), 1), (dict(cv=NULL), 1), (dict(sel=NULL), 1),
+    (dict(ck=ctypes.c_void_p(0x1008)), 2), (dict(pos=ctypes.c_void_p(0x1002)), 2),
+])
+def test_pack_rejects(L, kw, status):
+    from paper_2607_21848_amd import _lib
+    assert _pack(L, **kw) == status
+    assert len(_lib.last_error()) > 0
+
+
+def test_pack_nothing_to_do_is_ok(L):
+    assert _pack(L, n_sel=0, sel=NULL, ck=NULL, cv=NULL) == 0
+    assert _pack(L, layers=0, sel=NULL) == 0
+    # rope_theta is not looked at without temporal pairs
+    assert _pack(L, n_sel=0, nt=0, theta=0.0) == 0
