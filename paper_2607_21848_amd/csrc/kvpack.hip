@@ -6,9 +6,10 @@
 //
 // The work is a stream: every byte is read once and written once, so the
 // kernel is bound by HBM and is laid out for it. One 256-thread block moves
-// 32 KiB of one (layer, slot, K or V) chunk image: eight 16-byte vectors per
+// 16 KiB of one (layer, slot, K or V) chunk image: four 16-byte vectors per
 // thread, block-strided so that every load and store instruction covers 4 KiB
-// of consecutive bytes, all eight loads in flight before the first use.
+// of consecutive bytes, all four loads in flight before the first use (more
+// per thread, or larger blocks, measured slower).
 // Loads and stores are non-temporal: neither side is reused by this kernel,
 // and the store is far larger than the caches.
 //
@@ -37,7 +38,7 @@ namespace revisit {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kVecsPerThread = 8;
+constexpr int kVecsPerThread = 4;
 constexpr int kSpan = kBlock * kVecsPerThread;  // 16-byte vectors per block
 constexpr int kMaxPairs = 256;                  // D <= 512
 

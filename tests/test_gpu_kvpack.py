@@ -118,7 +118,7 @@ def test_pack_small(dtype, D, n_t):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_pack_ragged_blocks_and_default_positions(dtype):
-    # chunk images of 7*11*2*H*D elements: not a multiple of one block's 32 KiB
+    # chunk images of 7*11*2*H*D elements: not a multiple of one block's 16 KiB
     rng = np.random.default_rng(21)
     L, n_store, F, h, w, H, D, n_t = 3, 9, 2, 7, 11, 5, 72, 13
     T = F * h * w
