@@ -672,13 +672,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // 1 = d = 3, 2 = d = 2 (tile j + 1 is the last), 3 = d = 1 (tile j is the last).
     // Loads issued in step j - 1 may stay in flight: each lane waits only for
     // those of step j - 2, which carried K_{j+1} and V_j.
-    auto step = [&](auto phase_tag, auto kind_tag, int j) {
-        constexpr int P = decltype(phase_tag)::value;
+    // The body takes the ring slots (knext: the slot holding K_{j+1} and V_j;
+    // refill: this wave's part of slot j mod 3) and the logit buffers as
+    // arguments: compile-time in the steady loop, chosen at run time in the
+    // last few steps.
+    auto step_core = [&](auto kind_tag, int j, floatx16& S_cur, floatx16& S_next, const uint8_t* knext,
+                         const uint32_t refill) __attribute__((always_inline)) {
         constexpr int kind = decltype(kind_tag)::value;
         constexpr bool has_next = kind != 3;
-        floatx16& S_cur = (P & 1) ? Sb : Sa;
-        floatx16& S_next = (P & 1) ? Sa : Sb;
-        const uint8_t* knext = ring(std::integral_constant<int, P + 1>{});
         const uint8_t* vcur = knext + kTileBytes;
         // this lane's loads issued in step j - 1: K_{j+2} if it exists, V_{j+1} if it exists
         if constexpr (kind <= 1) {
@@ -689,7 +690,6 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             __builtin_amdgcn_s_waitcnt(kWaitVm0);
         }
         wg_barrier();
-        const uint32_t refill = dst(std::integral_constant<int, P>{});
         if constexpr (kind == 0) load_tile_lds(Kg, refill, (t0 + j + 3) * kTK, Lk, row_stride, tl, hd, wave, lane);
         if constexpr (kind <= 1) load_tile_lds(Vg, refill + kTileBytes, (t0 + j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
 
@@ -795,6 +795,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         }
         mx_cur = mx_next;
     };
+    auto step = [&](auto phase_tag, auto kind_tag, int j) __attribute__((always_inline)) {
+        constexpr int P = decltype(phase_tag)::value;
+        step_core(kind_tag, j, (P & 1) ? Sb : Sa, (P & 1) ? Sa : Sb, ring(std::integral_constant<int, P + 1>{}),
+                  dst(std::integral_constant<int, P>{}));
+    };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
@@ -819,33 +824,23 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         step(I4{}, I0{}, j + 4);
         step(I5{}, I0{}, j + 5);
     }
-    // the last 1 .. 8 tiles, starting at phase 0: full-loading steps while
-    // d > 3, then the three ending kinds; phases continue modulo 6
-    const int left = nt - j;
-    auto ending = [&](auto p_tag) {
-        constexpr int P = decltype(p_tag)::value;
-        step(std::integral_constant<int, P % 6>{}, I1{}, nt - 3);
-        step(std::integral_constant<int, (P + 1) % 6>{}, I2{}, nt - 2);
-        step(std::integral_constant<int, (P + 2) % 6>{}, I3{}, nt - 1);
+    // the last 1 .. 8 tiles: one copy of the step body per kind, ring slot
+    // chosen at run time. The steady loop leaves off at a multiple of six, so
+    // step j refills slot 0 and the logits of tile j are in Sa; after each
+    // step the logits of tile j + 1 move from Sb to Sa.
+    auto slot_base = [&](int slot) -> const uint8_t* { return slot == 0 ? lds_r0 : (slot == 1 ? lds_r1 : lds_r2); };
+    int slot = 0;
+    auto tail_step = [&](auto kind_tag) __attribute__((always_inline)) {
+        const int nxt = slot == 2 ? 0 : slot + 1;
+        step_core(kind_tag, j, Sa, Sb, slot_base(nxt), lds_addr(slot_base(slot)) + wave_off);
+        if constexpr (decltype(kind_tag)::value != 3) Sa = Sb;
+        slot = nxt;
+        ++j;
     };
-    if (left >= 4) step(I0{}, I0{}, j);
-    if (left >= 5) step(I1{}, I0{}, j + 1);
-    if (left >= 6) step(I2{}, I0{}, j + 2);
-    if (left >= 7) step(I3{}, I0{}, j + 3);
-    if (left >= 8) step(I4{}, I0{}, j + 4);
-    switch (left) {
-        case 1: step(I0{}, I3{}, j); break;
-        case 2:
-            step(I0{}, I2{}, j);
-            step(I1{}, I3{}, j + 1);
-            break;
-        case 3: ending(I0{}); break;
-        case 4: ending(I1{}); break;
-        case 5: ending(I2{}); break;
-        case 6: ending(I3{}); break;
-        case 7: ending(I4{}); break;
-        default: ending(I5{}); break;
-    }
+    while (nt - j > 3) tail_step(I0{});
+    if (nt - j == 3) tail_step(I1{});
+    if (nt - j == 2) tail_step(I2{});
+    tail_step(I3{});
 
     const float l_tot = half_swap_sum(l_run0 + l_run1);
     if (t0 == 0 && nt == n_tiles) {
