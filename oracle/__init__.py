@@ -21,6 +21,9 @@ Modules, each citing the passage of the paper it writes out:
   of their keys and values and re-rotation of the keys' temporal position
   embedding to the packed positions (Sec. 4.2, cache layout and cache
   packing);
+* ``stream``       -- the cache layout run chunk by chunk over a trajectory:
+  history ring, retrieval, slot table, correspondence, packing and biased
+  attention composed as the method runs them (Sec. 4.2, Sec. 4.3);
 * ``brute``        -- pure-Python loop versions of the first three, for tiny
   inputs, used to pin the vectorised ones.
 
@@ -28,4 +31,4 @@ Every function here has pins in ``tests/test_oracle_*.py`` (closed forms,
 invariants, library reductions, brute force); none is "parity unpinned".
 """
 
-from . import attention, brute, kvpack, reprojection, retrieval  # noqa: F401
+from . import attention, brute, kvpack, reprojection, retrieval, stream  # noqa: F401
