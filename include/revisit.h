@@ -19,14 +19,18 @@
  *                                values into the cache, keys re-rotated to
  *                                the packed positions (Sec. 4.2)
  *
+ * and a streaming driver (rc_stream_*) that runs the paper's cache layout
+ * chunk by chunk on the device.
+ *
  * Conventions common to all entry points
  * --------------------------------------
  * - Every array argument is a DEVICE pointer owned by the caller and must
  *   stay valid until the work queued on `stream` has completed. Outputs must
  *   not alias inputs. State kept by the library: a per-thread last-error
- *   string, the setting of rc_set_attention_key_parts(), and the bf16
- *   attention workspace described at biased_chunk_attention (the only
- *   device memory it allocates).
+ *   string, the setting of rc_set_attention_key_parts(), the bf16
+ *   attention workspace described at biased_chunk_attention, and the
+ *   device memory of stream objects (rc_stream_create), which the caller
+ *   owns through the handle.
  * - Calls are asynchronous on `stream` (NULL = the default stream).
  * - Arguments are validated on the host before anything is queued: on a
  *   non-zero status nothing has been enqueued and rc_last_error() says why.
@@ -58,7 +62,8 @@ enum {
     REVISIT_ERR_SHAPE = 2,       /* a size is negative, inconsistent or too large */
     REVISIT_ERR_UNSUPPORTED = 3, /* dtype / head dimension not built */
     REVISIT_ERR_PARAM = 4,       /* a method parameter is out of its domain */
-    REVISIT_ERR_LAUNCH = 5       /* the HIP runtime refused the launch */
+    REVISIT_ERR_LAUNCH = 5,      /* the HIP runtime refused the launch */
+    REVISIT_ERR_MEMORY = 6       /* a stream object could not get its memory */
 };
 
 /* Element types of biased_chunk_attention. */
@@ -266,6 +271,96 @@ int pack_retrieved_kv(const void* store_k, const void* store_v,
                       int32_t F, int32_t h, int32_t w, int32_t H, int32_t D,
                       int32_t rope_t_pairs, float rope_theta,
                       hipStream_t stream);
+
+/*
+ * Streaming driver -- Sec. 4.2 (cache layout, loop-closure retrieval, cache
+ * packing) and Sec. 4.3, run chunk by chunk over one generated sequence.
+ *
+ * A stream object owns the device memory of the sequence: the pose bank
+ * (max_chunks poses), the history ring and the packed attention cache. The
+ * ring keeps the anchor and the capacity - 1 newest chunks: per chunk the
+ * pre-pooled token depth, the frame poses, the token-grid intrinsics (K / p)
+ * and every layer's keys and values. Chunk m >= 1 lives at ring slot
+ * 1 + (m - 1) mod (capacity - 1). rc_stream_step() runs chunk n = 0, 1, 2, ...
+ * and enqueues everything on `stream` without host synchronisation:
+ *   1. the chunk enters the ring (depth pooled to the token grid: p x p mean
+ *      in double rounded to fp32) and its middle frame's pose the bank;
+ *   2. retrieval (Eq. retrieval, k = 1) over the resident chunks 1..n-1,
+ *      i.e. first candidate max(1, n - capacity + 2);
+ *   3. the layout of the attention range, in this order and with these frame
+ *      positions: anchor chunk 0 (0..F-1), the retrieved chunk (F..2F-1) --
+ *      or, when nothing is admissible, chunk n-3 as the extension of the
+ *      recent window, unbiased --, recent chunks n-2 (2F..) and n-1 (3F..),
+ *      and the current chunk (4F..5F-1); parts that do not exist yet are
+ *      left out (the retrieved slot exists from n = 4 on). The retrieved
+ *      part's ring slot, the KV frame slot table and the source frames of
+ *      step 4 are built on the device from the retrieval result;
+ *   4. correspondence (Eq. reprojection, Eq. visibility) of the chunk's tokens
+ *      into the retrieved chunk's F frames, on the pooled maps (p = 1);
+ *   5. the packed cache of every layer (pack_retrieved_kv; keys enter the
+ *      ring with the embedding of position 4F + f, as the network produced
+ *      them for the current role, and are re-rotated to their role's
+ *      position);
+ *   6. biased attention (Eq. bias) of every layer over its packed cache,
+ *      the retrieved frames carrying slots 0..F-1 when a chunk was retrieved.
+ *
+ * rc_stream_create -- allocates the stream on the current device.
+ *   dtype REVISIT_BF16 (D = 128) or REVISIT_F32 (D = 64 or 128); 1 <= F <= 64;
+ *   capacity >= 5 (keeps chunk n-3 resident); method parameters as for the
+ *   stage entry points. Allocation failure: REVISIT_ERR_MEMORY, nothing kept.
+ *   Device memory: layers * capacity * F h w * H * D * 2 (K and V) elements
+ *   for the ring plus layers * 5 F h w * H * D * 2 for the cache, plus small
+ *   tables.
+ * rc_stream_step -- runs the next chunk. Inputs (device, caller-owned):
+ *   depth [F][h p][w p] fp32 planar depth, c2w [F][4][4], K [F][4] depth-pixel
+ *   intrinsics; q, k, v [layers][F h w][H][D] in dtype (k with the rotary
+ *   embedding of positions 4F + f); outputs o [layers][F h w][H][D] and lse
+ *   (nullable) [layers][H][F h w]. The device must be the one the stream was
+ *   created on. Steps of one stream must be issued in order on one stream
+ *   (they share the object's buffers); REVISIT_ERR_SHAPE once max_chunks
+ *   chunks have run.
+ * rc_stream_view -- device pointers to the last step's intermediate results
+ *   (retrieval, layout tables, correspondence, packed cache) and its layout
+ *   sizes, for inspection; valid until the next step or rc_stream_destroy.
+ * rc_stream_destroy -- waits for the device and frees everything (NULL: no-op).
+ */
+typedef struct rc_stream rc_stream;
+
+typedef struct {
+    int32_t F, h, w, p;           /* frames per chunk, token grid, depth pixels per token side */
+    int32_t H, D, layers, dtype;  /* heads, head dim, transformer layers, REVISIT_BF16 / REVISIT_F32 */
+    int32_t capacity;             /* history ring chunks, >= 5 */
+    int32_t max_chunks;           /* pose bank length: chunks the stream may run */
+    float E, w_v, tau_c, tau_v;   /* retrieval (Eq. retrieval), tau_v in radians */
+    int32_t delta;                /* temporal gap gate */
+    float eps, lambda, sigma, softmax_scale;  /* visibility tolerance and bias (Sec. 4.3) */
+    int32_t rope_t_pairs;         /* temporal pairs of the rotary embedding (0..D/2) */
+    float rope_theta;
+} rc_stream_config;
+
+typedef struct {
+    int32_t n;          /* chunk id of the last step, -1 before the first */
+    int32_t n_parts;    /* parts of its attention range, in layout order */
+    int32_t ret_part;   /* index of the retrieved / extension part, -1 if absent */
+    int32_t Lk;         /* keys per layer: n_parts F h w */
+    int32_t cache_rows; /* rows per layer of the cache arrays: 5 F h w */
+    const int32_t* ret_idx;    /* [1] retrieved chunk or -1 (n >= 1) */
+    const int32_t* ret_count;  /* [1] 0 or 1 (n >= 1) */
+    const int32_t* part_slot;  /* [n_parts] ring slot of every part */
+    const int32_t* kv_slot;    /* [n_parts F] KV frame slot table */
+    const int32_t* src_sel;    /* [F] ring frames of the retrieved chunk, or -1 */
+    const float* corr_uv;      /* [F][F h w][2] (ret_part >= 0) */
+    const int32_t* corr_idx;   /* [F][F h w]    (ret_part >= 0) */
+    const void* cache_k;       /* [layers][cache_rows][H][D], first Lk rows valid */
+    const void* cache_v;
+} rc_stream_state;
+
+int rc_stream_create(const rc_stream_config* cfg, rc_stream** out);
+int rc_stream_step(rc_stream* s, const float* depth, const float* c2w, const float* K,
+                   const void* q, const void* k, const void* v, void* o, float* lse,
+                   hipStream_t stream);
+int rc_stream_view(const rc_stream* s, rc_stream_state* out);
+int rc_stream_destroy(rc_stream* s);
 
 /*
  * rc_set_attention_key_parts -- tuning knob of the bf16 attention work split

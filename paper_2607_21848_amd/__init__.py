@@ -26,7 +26,7 @@ from . import _lib
 from ._lib import BF16, F32, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
 
 __all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "pack_retrieved_kv",
-           "set_attention_key_parts",
+           "StreamDriver", "set_attention_key_parts",
            "RevisitError", "lib"]
 
 
@@ -211,6 +211,76 @@ def pack_retrieved_kv(store_k: torch.Tensor, store_v: torch.Tensor, sel: torch.T
                                  int(dst_pos), _ptr(cache_k), _ptr(cache_v), int(dst_row0), rows, L, dt, F, h, w, H,
                                  D, int(rope_t_pairs), float(rope_theta), _stream(dev))
     _lib.check("pack_retrieved_kv", st)
+
+
+class StreamDriver:
+    """The paper's cache layout run chunk by chunk on the device (rc_stream_*).
+
+    Owns a stream object: history ring of ``capacity`` chunks, pose bank of
+    ``max_chunks``, packed cache. ``step`` runs the next chunk: depth
+    [F, h*p, w*p] f32, c2w [F, 4, 4] f32, K [F, 4] f32, q, k, v
+    [layers, F*h*w, H, D] (bf16 or f32, k embedded at positions 4F + f);
+    returns o [layers, F*h*w, H, D] and lse [layers, H, F*h*w]."""
+
+    def __init__(self, *, F: int, h: int, w: int, p: int, H: int, D: int, layers: int, dtype: torch.dtype,
+                 capacity: int, max_chunks: int, E: float, w_v: float, tau_c: float, tau_v: float, delta: int,
+                 eps: float, lam: float, sigma: float, softmax_scale: float, rope_t_pairs: int, rope_theta: float):
+        if dtype == torch.bfloat16:
+            dt = BF16
+        elif dtype == torch.float32:
+            dt = F32
+        else:
+            raise TypeError(f"dtype must be bfloat16 or float32 (got {dtype})")
+        self.dtype = dtype
+        self.F, self.h, self.w, self.p, self.H, self.D, self.layers = F, h, w, p, H, D, layers
+        cfg = _lib.StreamConfig(F=F, h=h, w=w, p=p, H=H, D=D, layers=layers, dtype=dt, capacity=capacity,
+                                max_chunks=max_chunks, E=E, w_v=w_v, tau_c=tau_c, tau_v=tau_v, delta=delta, eps=eps,
+                                lam=lam, sigma=sigma, softmax_scale=softmax_scale, rope_t_pairs=rope_t_pairs,
+                                rope_theta=rope_theta)
+        handle = ctypes.c_void_p(0)
+        _lib.check("rc_stream_create", lib().rc_stream_create(ctypes.byref(cfg), ctypes.byref(handle)))
+        self._h = handle
+
+    def step(self, depth, c2w, K, q, k, v, out=None):
+        if not self._h:
+            raise RuntimeError("stream already closed")
+        dev = q.device
+        T = self.F * self.h * self.w
+        _need(depth, "depth", torch.float32, (self.F, self.h * self.p, self.w * self.p), dev)
+        _need(c2w, "c2w", torch.float32, (self.F, 4, 4), dev)
+        _need(K, "K", torch.float32, (self.F, 4), dev)
+        shape = (self.layers, T, self.H, self.D)
+        for t, name in ((q, "q"), (k, "k"), (v, "v")):
+            _need(t, name, self.dtype, shape, dev)
+        if out is None:
+            o = torch.empty(shape, dtype=self.dtype, device=dev)
+            lse = torch.empty((self.layers, self.H, T), dtype=torch.float32, device=dev)
+        else:
+            o, lse = out
+            _need(o, "o", self.dtype, shape, dev)
+            if lse is not None:
+                _need(lse, "lse", torch.float32, (self.layers, self.H, T), dev)
+        st = lib().rc_stream_step(self._h, _ptr(depth), _ptr(c2w), _ptr(K), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                  _ptr(lse), _stream(dev))
+        _lib.check("rc_stream_step", st)
+        return o, lse
+
+    def state(self):
+        """The last step's layout sizes and device pointers (rc_stream_state)."""
+        stt = _lib.StreamState()
+        _lib.check("rc_stream_view", lib().rc_stream_view(self._h, ctypes.byref(stt)))
+        return stt
+
+    def close(self):
+        if self._h:
+            lib().rc_stream_destroy(self._h)
+            self._h = ctypes.c_void_p(0)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def set_attention_key_parts(parts: int) -> None:

@@ -13,15 +13,32 @@ import os
 _LIB = None
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librevisit.so")
 
-OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH = 0, 1, 2, 3, 4, 5
+OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH, ERR_MEMORY = 0, 1, 2, 3, 4, 5, 6
 BF16, F32 = 1, 2
 MAX_K = 32
 EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
-            "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv")
+            "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv", "rc_stream_create",
+            "rc_stream_step", "rc_stream_view", "rc_stream_destroy")
 
 _p = ctypes.c_void_p
 _i = ctypes.c_int32
 _f = ctypes.c_float
+
+
+class StreamConfig(ctypes.Structure):
+    """rc_stream_config of include/revisit.h."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("F", "h", "w", "p", "H", "D", "layers", "dtype", "capacity",
+                                               "max_chunks")] + \
+               [(n, ctypes.c_float) for n in ("E", "w_v", "tau_c", "tau_v")] + [("delta", ctypes.c_int32)] + \
+               [(n, ctypes.c_float) for n in ("eps", "lam", "sigma", "softmax_scale")] + \
+               [("rope_t_pairs", ctypes.c_int32), ("rope_theta", ctypes.c_float)]
+
+
+class StreamState(ctypes.Structure):
+    """rc_stream_state of include/revisit.h."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("n", "n_parts", "ret_part", "Lk", "cache_rows")] + \
+               [(n, ctypes.c_void_p) for n in ("ret_idx", "ret_count", "part_slot", "kv_slot", "src_sel", "corr_uv",
+                                               "corr_idx", "cache_k", "cache_v")]
 
 
 class RevisitError(RuntimeError):
@@ -53,6 +70,14 @@ def lib() -> ctypes.CDLL:
         L.pack_retrieved_kv.restype = ctypes.c_int
         L.pack_retrieved_kv.argtypes = [_p, _p, _p, _i, _p, _i, _i, _p, _p, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
                                         _f, _p]
+        L.rc_stream_create.restype = ctypes.c_int
+        L.rc_stream_create.argtypes = [ctypes.POINTER(StreamConfig), ctypes.POINTER(ctypes.c_void_p)]
+        L.rc_stream_step.restype = ctypes.c_int
+        L.rc_stream_step.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
+        L.rc_stream_view.restype = ctypes.c_int
+        L.rc_stream_view.argtypes = [_p, ctypes.POINTER(StreamState)]
+        L.rc_stream_destroy.restype = ctypes.c_int
+        L.rc_stream_destroy.argtypes = [_p]
         L.rc_set_attention_key_parts.restype = ctypes.c_int
         L.rc_set_attention_key_parts.argtypes = [_i]
         _LIB = L

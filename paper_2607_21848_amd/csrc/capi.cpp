@@ -1,7 +1,7 @@
 // C entry points of librevisit: argument validation on the host, then the
 // kernel launches on the caller's stream. State: a per-thread last-error
 // string, the bf16 attention key-part setting, and the attention workspace
-// (workspace.cpp).
+// (workspace.cpp). The streaming driver's entry points are in stream.cpp.
 
 #include <math.h>
 #include <stdarg.h>
@@ -45,6 +45,16 @@ std::atomic<int> g_attention_key_parts{0};
 
 }  // namespace
 
+namespace revisit {
+int fail_status(int status, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return status;
+}
+}  // namespace revisit
+
 extern "C" {
 
 const char* rc_status_string(int status) {
@@ -55,6 +65,7 @@ const char* rc_status_string(int status) {
         case REVISIT_ERR_UNSUPPORTED: return "unsupported";
         case REVISIT_ERR_PARAM: return "bad parameter";
         case REVISIT_ERR_LAUNCH: return "launch error";
+        case REVISIT_ERR_MEMORY: return "out of memory";
         default: return "unknown status";
     }
 }

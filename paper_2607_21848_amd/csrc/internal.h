@@ -114,7 +114,41 @@ struct KvPackArgs {
 int64_t kvpack_blocks(const KvPackArgs& a);
 hipError_t launch_kvpack(const KvPackArgs& a, hipStream_t stream);
 
+// Streaming driver device steps (stream_kernels.hip).
+struct StreamCommitArgs {
+    const float* depth;  // [F][h p][w p]
+    const float* c2w;    // [F][4][4]
+    const float* K;      // [F][4] depth-pixel intrinsics
+    int32_t F, h, w, p;
+    int32_t n;     // chunk id
+    int32_t slot;  // its ring slot
+    float* ring_depth;  // [C][F][h][w]
+    float* ring_c2w;    // [C][F][4][4]
+    float* ring_K;      // [C][F][4] token-grid intrinsics
+    float* bank;        // [max_chunks][4][4] representative poses
+    int32_t* query_chunk;
+};
+hipError_t launch_stream_commit(const StreamCommitArgs& a, hipStream_t stream);
+
+constexpr int kStreamMaxParts = 5;
+struct StreamSlotsArgs {
+    int32_t n, F, capacity;
+    int32_t n_parts;
+    int32_t ret_part;  // index of the retrieved / extension part, -1 if absent
+    int32_t has_ret;
+    int32_t part_chunk[kStreamMaxParts];  // chunk of every other part
+    const int32_t* ret_idx;
+    const int32_t* ret_count;
+    int32_t* part_slot;  // [n_parts] ring slots in layout order
+    int32_t* kv_slot;    // [n_parts * F]
+    int32_t* src_sel;    // [F]
+};
+hipError_t launch_stream_slots(const StreamSlotsArgs& a, hipStream_t stream);
+
 hipError_t stream_workspace(hipStream_t stream, size_t bytes, void** out);
+
+// Sets the calling thread's last-error string and returns status (capi.cpp).
+int fail_status(int status, const char* fmt, ...);
 hipError_t device_compute_units(int* cus);
 
 }  // namespace revisit

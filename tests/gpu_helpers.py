@@ -47,3 +47,20 @@ def same_bits_f32(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     a = np.asarray(a, np.float32)
     b = np.asarray(b, np.float32)
     return (a.view(np.uint32) == b.view(np.uint32)) | (np.isnan(a) & np.isnan(b))
+
+
+_HIP = None
+
+
+def read_device(ptr: int, nbytes: int) -> np.ndarray:
+    """Bytes at a raw device pointer (after the work producing them has finished)."""
+    global _HIP
+    import ctypes
+    if _HIP is None:
+        _HIP = ctypes.CDLL("libamdhip64.so")
+        _HIP.hipMemcpy.restype = ctypes.c_int
+        _HIP.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+    out = np.empty(nbytes, np.uint8)
+    if nbytes:
+        assert _HIP.hipMemcpy(out.ctypes.data, ptr, nbytes, 2) == 0  # device to host
+    return out

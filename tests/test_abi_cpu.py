@@ -162,3 +162,32 @@ def test_pack_nothing_to_do_is_ok(L):
     assert _pack(L, layers=0, sel=NULL) == 0
     # rope_theta is not looked at without temporal pairs
     assert _pack(L, n_sel=0, nt=0, theta=0.0) == 0
+
+
+def _stream_cfg(**kw):
+    from paper_2607_21848_amd import _lib
+    a = dict(F=3, h=30, w=52, p=2, H=12, D=128, layers=30, dtype=1, capacity=16, max_chunks=100, E=40.0, w_v=0.5,
+             tau_c=0.05, tau_v=0.785, delta=3, eps=0.05, lam=1.0, sigma=2.0, softmax_scale=0.088, rope_t_pairs=22,
+             rope_theta=10000.0)
+    a.update(kw)
+    return _lib.StreamConfig(**a)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=5), 3), (dict(D=64), 3), (dict(dtype=2, D=96), 3), (dict(F=0), 2), (dict(F=65), 2), (dict(h=0), 2),
+    (dict(layers=0), 2), (dict(capacity=4), 2), (dict(max_chunks=0), 2), (dict(E=0.0), 4),
+    (dict(sigma=float("nan")), 4), (dict(eps=-1.0), 4), (dict(softmax_scale=0.0), 4), (dict(rope_t_pairs=65), 4),
+    (dict(rope_theta=-1.0), 4),
+])
+def test_stream_create_rejects(L, kw, status):
+    h = ctypes.c_void_p(0x1234)
+    assert L.rc_stream_create(ctypes.byref(_stream_cfg(**kw)), ctypes.byref(h)) == status
+    assert not h.value  # *out cleared on failure
+
+
+def test_stream_null_arguments(L):
+    h = ctypes.c_void_p(0)
+    assert L.rc_stream_create(None, ctypes.byref(h)) == 1
+    assert L.rc_stream_step(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NULL, NULL) == 1
+    assert L.rc_stream_view(None, None) == 1
+    assert L.rc_stream_destroy(None) == 0

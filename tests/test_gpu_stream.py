@@ -1,0 +1,129 @@
+"""GPU parity of the streaming driver (rc_stream_*) against the streaming oracle.
+
+The driver runs the loop trajectory chunk by chunk. Every chunk is checked
+against the oracle, stage by stage, from the driver's own buffers:
+* retrieval result and layout (parts, ring slots, KV frame slot table):
+  exact;
+* correspondence codes and u^: bit-exact (both sides evaluate the same IEEE
+  double expressions on the same fp32 pooled maps);
+* packed cache: values bit for bit, keys bit-exact in bf16 and within 1 ulp
+  in fp32 (as for pack_retrieved_kv);
+* attention output and LSE: the bars of biased_chunk_attention (1e-4 fp32;
+  2e-2 / 2e-3 bf16).
+Capacities 10 (loop closures retrieved on the second lap) and 6 (the ring has
+evicted the revisited chunks: the retrieved slot extends the recent window).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_21848_amd as rv
+from oracle.stream import StreamOracle
+from tests.gpu_helpers import read_device
+from workloads.stream import make_stream
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rv.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _dev(a: np.ndarray, bf16: bool = False) -> torch.Tensor:
+    if bf16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _ordered(a: np.ndarray) -> np.ndarray:
+    if a.dtype == np.uint16:
+        i = a.astype(np.int64)
+        return np.where(i & 0x8000, 0x8000 - i, i)
+    i = a.view(np.uint32).astype(np.int64)
+    return np.where(i & 0x80000000, 0x80000000 - i, i)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("capacity", [10, 6])
+def test_stream_against_oracle(dtype, capacity):
+    st = make_stream(n_chunks=14, dtype=dtype)
+    bf16 = dtype == "bf16"
+    orc = StreamOracle(st, capacity)
+    drv = rv.StreamDriver(F=st.F, h=st.h, w=st.w, p=st.p, H=st.H, D=st.D, layers=st.L,
+                          dtype=torch.bfloat16 if bf16 else torch.float32, capacity=capacity, max_chunks=64, E=st.E,
+                          w_v=st.w_v, tau_c=st.tau_c, tau_v=st.tau_v, delta=st.delta, eps=st.eps, lam=st.lam,
+                          sigma=st.sigma, softmax_scale=st.softmax_scale, rope_t_pairs=st.rope_t_pairs,
+                          rope_theta=st.rope_theta)
+    T = st.F * st.h * st.w
+    esize = 2 if bf16 else 4
+    o_tol, l_tol = (2e-2, 2e-3) if bf16 else (1e-4, 1e-4)
+    retrieved = 0
+    try:
+        for n, ch in enumerate(st.chunks):
+            o, lse = drv.step(_dev(ch.depth), _dev(ch.c2w), _dev(ch.K), _dev(ch.q, bf16), _dev(ch.k, bf16),
+                              _dev(ch.v, bf16))
+            torch.cuda.synchronize()
+            want = orc.step(n)
+            s = drv.state()
+            assert (s.n, s.n_parts, s.Lk) == (n, len(want["parts"]), len(want["parts"]) * T)
+            roles = [r for r, _, _ in want["parts"]]
+            assert s.ret_part == (roles.index("retrieved") if "retrieved" in roles else
+                                  roles.index("extension") if "extension" in roles else -1)
+            if n >= 1:
+                cnt = int(read_device(s.ret_count, 4).view(np.int32)[0])
+                idx = int(read_device(s.ret_idx, 4).view(np.int32)[0])
+                assert cnt == want["count"] and (cnt == 0 or idx == want["idx"])
+                retrieved += cnt
+            slots = read_device(s.part_slot, 4 * s.n_parts).view(np.int32)
+            assert list(slots) == [orc.ring_slot(m) for _, m, _ in want["parts"]]
+            kv_slot = read_device(s.kv_slot, 4 * s.n_parts * st.F).view(np.int32)
+            assert np.array_equal(kv_slot, want["slot"])
+            if s.ret_part >= 0:
+                uv = read_device(s.corr_uv, st.F * T * 8).view(np.uint32).reshape(st.F, T, 2)
+                cidx = read_device(s.corr_idx, st.F * T * 4).view(np.int32).reshape(st.F, T)
+                assert np.array_equal(cidx, want["cidx"])
+                assert np.array_equal(uv, want["uv"].view(np.uint32))
+            row = st.H * st.D * esize
+            ck = read_device(s.cache_k, st.L * s.cache_rows * row).reshape(st.L, s.cache_rows, -1)[:, :s.Lk]
+            cv = read_device(s.cache_v, st.L * s.cache_rows * row).reshape(st.L, s.cache_rows, -1)[:, :s.Lk]
+            view = np.uint16 if bf16 else np.float32
+            ck = np.ascontiguousarray(ck).view(view).reshape(want["cache_k"].shape)
+            cv = np.ascontiguousarray(cv).view(view).reshape(want["cache_v"].shape)
+            assert cv.tobytes() == want["cache_v"].tobytes()
+            d = np.abs(_ordered(ck) - _ordered(want["cache_k"]))
+            assert int(d.max()) <= (0 if bf16 else 1)
+            got_o = o.float().cpu().numpy()
+            assert np.abs(got_o - want["o"]).max() <= o_tol
+            assert np.abs(lse.cpu().numpy() - want["lse"]).max() <= l_tol
+    finally:
+        drv.close()
+    if capacity == 10:
+        assert retrieved == 5  # chunks 9..13 revisit chunks 1..5
+    else:
+        assert retrieved == 0
+
+
+def test_stream_runs_out_of_bank():
+    st = make_stream(n_chunks=3, dtype="f32")
+    drv = rv.StreamDriver(F=st.F, h=st.h, w=st.w, p=st.p, H=st.H, D=st.D, layers=st.L, dtype=torch.float32,
+                          capacity=5, max_chunks=2, E=st.E, w_v=st.w_v, tau_c=st.tau_c, tau_v=st.tau_v,
+                          delta=st.delta, eps=st.eps, lam=st.lam, sigma=st.sigma, softmax_scale=st.softmax_scale,
+                          rope_t_pairs=st.rope_t_pairs, rope_theta=st.rope_theta)
+    try:
+        for n in range(2):
+            ch = st.chunks[n]
+            drv.step(_dev(ch.depth), _dev(ch.c2w), _dev(ch.K), _dev(ch.q), _dev(ch.k), _dev(ch.v))
+        ch = st.chunks[2]
+        with pytest.raises(rv.RevisitError) as e:
+            drv.step(_dev(ch.depth), _dev(ch.c2w), _dev(ch.K), _dev(ch.q), _dev(ch.k), _dev(ch.v))
+        assert e.value.status == 2
+    finally:
+        drv.close()
