@@ -15,7 +15,8 @@ throughput of a batched launch (1024 independent problems, > 2x the 256 MB
 last-level cache), retrieval latency, the retrieval bandwidth on a stress
 bank, and the cache packing of the step's retrieved chunks for all 30
 layers from a store of every bank chunk's keys and values (HBM-bound, not
-part of the step); ``cpu_baseline`` times the fp64
+part of the step), and the streaming driver's per-chunk time for the paper's
+cache layout over all 30 layers; ``cpu_baseline`` times the fp64
 oracle on a bounded sample of the same workload on this host.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
@@ -43,6 +44,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 BENCH_QUERY = 1  # query chunk n = 225: a full top-4 retrieval
 PACK_LAYERS = 30  # transformer blocks of the 1.3B backbone: one packing call covers all of them
 ROPE_T_PAIRS, ROPE_THETA = 22, 10000.0  # temporal band of the factorised 3-D RoPE at head dim 128
+STREAM_CHUNKS, STREAM_CAPACITY, STREAM_TIMED_FROM = 14, 16, 9  # chunks 9..13 retrieve the first lap
 REPROJ_BATCH = 1024
 
 
@@ -279,6 +281,41 @@ def main():
     log(f"cache packing {pk_ms:.3f} ms: {pk_gbs:.0f} GB/s algorithmic")
     del store_k, store_v, cache_k, cache_v
 
+    torch.cuda.empty_cache()  # hand the packing store back before the stream allocates its ring
+
+    # streaming driver: the paper's cache layout (anchor, 1 retrieved, 2 recent, current) chunk by chunk,
+    # all 30 layers, on a 14-chunk loop whose second lap revisits the first; per-chunk device time
+    from workloads.stream import make_stream
+    log("streaming driver: 14 chunks, 30 layers, history ring of 16 chunks")
+    sst = make_stream(n_chunks=STREAM_CHUNKS, h=wl.h, w=wl.w, p=wl.p, H=wl.H, D=wl.D, L=PACK_LAYERS, qkv=False)
+    Ts = sst.F * sst.h * sst.w
+    drv = rv.StreamDriver(F=sst.F, h=sst.h, w=sst.w, p=sst.p, H=sst.H, D=sst.D, layers=sst.L, dtype=torch.bfloat16,
+                          capacity=STREAM_CAPACITY, max_chunks=64, E=sst.E, w_v=sst.w_v, tau_c=sst.tau_c,
+                          tau_v=sst.tau_v, delta=sst.delta, eps=sst.eps, lam=sst.lam, sigma=sst.sigma,
+                          softmax_scale=sst.softmax_scale, rope_t_pairs=ROPE_T_PAIRS, rope_theta=ROPE_THETA)
+    gen.manual_seed(47)
+    sq, sk, sv = (torch.randn((sst.L, Ts, sst.H, sst.D), generator=gen, device=dev).to(torch.bfloat16)
+                  for _ in range(3))
+    so = torch.empty_like(sq)
+    slse = torch.empty((sst.L, sst.H, Ts), dtype=torch.float32, device=dev)
+    s_in = [(t(c.depth), t(c.c2w), t(c.K)) for c in sst.chunks]
+    s_ms, s_lk = [], []
+    for n, (d_, c_, k_) in enumerate(s_in):
+        e0.record(stream)
+        drv.step(d_, c_, k_, sq, sk, sv, out=(so, slse))
+        e1.record(stream)
+        torch.cuda.synchronize()
+        stt = drv.state()
+        if n >= STREAM_TIMED_FROM:
+            s_ms.append(e0.elapsed_time(e1))
+            s_lk.append(stt.Lk)
+    drv.close()
+    stream_ms = float(np.median(s_ms))
+    stream_flops = 4.0 * Ts * float(np.median(s_lk)) * sst.D * sst.H * sst.L
+    log(f"streaming driver: {stream_ms:.2f} ms per chunk (median of chunks {STREAM_TIMED_FROM}..{STREAM_CHUNKS - 1}), "
+        f"Lk {int(np.median(s_lk))}, attention {stream_flops / (stream_ms * 1e-3) / 1e12:.1f} TFLOP/s over the chunk")
+    del sq, sk, sv, so, slse, s_in
+
     counters = profiled_counters()
     out = {
         "metric": METRIC,
@@ -330,6 +367,14 @@ def main():
                 "rope_t_pairs": ROPE_T_PAIRS, "ms": round(pk_ms, 4), "bytes": pk_bytes,
                 "achieved_GBs": round(pk_gbs, 1), "peak_GBs": HBM_PEAK_GBS, "frac": round(pk_gbs / HBM_PEAK_GBS, 4),
                 "bound": "hbm", "traffic": counters.get("kvpack"),
+            },
+            "stream": {
+                "note": "paper cache layout per chunk: commit, retrieval (k = 1), slot tables, correspondence, "
+                        "packing and biased attention for every layer, one rc_stream_step",
+                "layers": PACK_LAYERS, "capacity": STREAM_CAPACITY, "chunks_timed": len(s_ms),
+                "Lk": int(np.median(s_lk)), "chunk_ms": round(stream_ms, 3),
+                "tokens_per_s": round(Ts / (stream_ms * 1e-3), 0),
+                "attention_tflops_per_chunk": round(stream_flops / (stream_ms * 1e-3) / 1e12, 2),
             },
             "retrieval_stress": {
                 "note": "stress bank outside the configs", "bank_poses": n_stress, "queries": 1, "top_k": 4,
