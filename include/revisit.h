@@ -273,6 +273,23 @@ int pack_retrieved_kv(const void* store_k, const void* store_v,
                       hipStream_t stream);
 
 /*
+ * pool_token_depth -- the query and source depth of Sec. 4.3 at token
+ * resolution (z_p = D_t(u_p) read per token), computed once per stored frame.
+ *
+ * out[f][r][c] = mean of the p x p block of depth pixels of token (r, c) of
+ * frame f, summed row-major (block row outer) in double and rounded to fp32
+ * once. Feeding pooled maps to reproject_correspondence with p = 1 and
+ * intrinsics divided by p reads 4 bytes of target depth per token instead of
+ * 4 p^2; where a block's mean is exact in fp32 the result is bit-identical to
+ * the full-resolution call.
+ *
+ *   depth [n_frames][h p][w p] fp32, out [n_frames][h][w] fp32 (4-byte aligned)
+ * n_frames == 0 is valid (nothing to do).
+ */
+int pool_token_depth(const float* depth, int32_t n_frames, int32_t h, int32_t w, int32_t p,
+                     float* out, hipStream_t stream);
+
+/*
  * Streaming driver -- Sec. 4.2 (cache layout, loop-closure retrieval, cache
  * packing) and Sec. 4.3, run chunk by chunk over one generated sequence.
  *

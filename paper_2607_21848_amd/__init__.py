@@ -26,7 +26,7 @@ from . import _lib
 from ._lib import BF16, F32, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
 
 __all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "pack_retrieved_kv",
-           "StreamDriver", "set_attention_key_parts",
+           "pool_token_depth", "StreamDriver", "set_attention_key_parts",
            "RevisitError", "lib"]
 
 
@@ -211,6 +211,21 @@ def pack_retrieved_kv(store_k: torch.Tensor, store_v: torch.Tensor, sel: torch.T
                                  int(dst_pos), _ptr(cache_k), _ptr(cache_v), int(dst_row0), rows, L, dt, F, h, w, H,
                                  D, int(rope_t_pairs), float(rope_theta), _stream(dev))
     _lib.check("pack_retrieved_kv", st)
+
+
+def pool_token_depth(depth: torch.Tensor, p: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Token depth [n, h, w] f32 from depth maps [n, h*p, w*p] f32 (p x p means, fp32)."""
+    dev = depth.device
+    if depth.dim() != 3 or depth.shape[1] % p or depth.shape[2] % p:
+        raise ValueError("depth must be [n, h*p, w*p]")
+    n, Hd, Wd = depth.shape
+    h, w = Hd // p, Wd // p
+    _need(depth, "depth", torch.float32, (n, Hd, Wd), dev)
+    if out is None:
+        out = torch.empty((n, h, w), dtype=torch.float32, device=dev)
+    _need(out, "out", torch.float32, (n, h, w), dev)
+    _lib.check("pool_token_depth", lib().pool_token_depth(_ptr(depth), n, h, w, p, _ptr(out), _stream(dev)))
+    return out
 
 
 class StreamDriver:

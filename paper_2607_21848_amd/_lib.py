@@ -17,7 +17,7 @@ OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH, ERR_MEMORY = 0,
 BF16, F32 = 1, 2
 MAX_K = 32
 EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
-            "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv", "rc_stream_create",
+            "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv", "pool_token_depth", "rc_stream_create",
             "rc_stream_step", "rc_stream_view", "rc_stream_destroy")
 
 _p = ctypes.c_void_p
@@ -70,6 +70,8 @@ def lib() -> ctypes.CDLL:
         L.pack_retrieved_kv.restype = ctypes.c_int
         L.pack_retrieved_kv.argtypes = [_p, _p, _p, _i, _p, _i, _i, _p, _p, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
                                         _f, _p]
+        L.pool_token_depth.restype = ctypes.c_int
+        L.pool_token_depth.argtypes = [_p, _i, _i, _i, _i, _p, _p]
         L.rc_stream_create.restype = ctypes.c_int
         L.rc_stream_create.argtypes = [ctypes.POINTER(StreamConfig), ctypes.POINTER(ctypes.c_void_p)]
         L.rc_stream_step.restype = ctypes.c_int

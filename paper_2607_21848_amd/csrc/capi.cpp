@@ -289,6 +289,19 @@ int pack_retrieved_kv(const void* store_k, const void* store_v, const int32_t* s
     return launched(revisit::launch_kvpack(a, stream), "pack_retrieved_kv");
 }
 
+int pool_token_depth(const float* depth, int32_t n_frames, int32_t h, int32_t w, int32_t p, float* out,
+                     hipStream_t stream) {
+    if (n_frames < 0 || h < 1 || w < 1 || p < 1)
+        return fail(REVISIT_ERR_SHAPE, "pool_token_depth: need n_frames >= 0 and h, w, p >= 1");
+    if ((int64_t)h * p > (1 << 20) || (int64_t)w * p > (1 << 20) ||
+        (double)n_frames * h * w * p * p > (double)kMaxElems)
+        return fail(REVISIT_ERR_SHAPE, "pool_token_depth: depth maps too large");
+    if (n_frames == 0) return REVISIT_OK;
+    if (!depth || !out) return fail(REVISIT_ERR_NULL, "pool_token_depth: depth and out are required");
+    if (!aligned(depth, 4) || !aligned(out, 4)) return fail(REVISIT_ERR_SHAPE, "pool_token_depth: arrays must be 4-byte aligned");
+    return launched(revisit::launch_pool_depth(depth, (int64_t)n_frames * h * w, h, w, p, out, stream), "pool_token_depth");
+}
+
 int rc_set_attention_key_parts(int32_t parts) {
     if (parts < 0 || parts > kMaxKeyParts)
         return fail(REVISIT_ERR_PARAM, "rc_set_attention_key_parts: %d outside [0, %d]", parts, kMaxKeyParts);

@@ -144,6 +144,8 @@ struct StreamSlotsArgs {
     int32_t* src_sel;    // [F]
 };
 hipError_t launch_stream_slots(const StreamSlotsArgs& a, hipStream_t stream);
+hipError_t launch_pool_depth(const float* depth, int64_t n_tokens, int32_t h, int32_t w, int32_t p, float* out,
+                             hipStream_t stream);
 
 hipError_t stream_workspace(hipStream_t stream, size_t bytes, void** out);
 

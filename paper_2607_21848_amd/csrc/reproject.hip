@@ -19,7 +19,8 @@
 // For the usual p = 2 the kernel is specialised: dividing by 2 or by 4 is
 // the same IEEE result as multiplying by 0.5 or 0.25, so the token-grid
 // intrinsics and the pooling mean cost a multiply instead of a division,
-// and each 2x2 depth block is read as two 8-byte loads.
+// and each 2x2 depth block is read as two 8-byte loads. p = 1 (maps pooled
+// beforehand, intrinsics already on the token grid) reads one value per token.
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -36,10 +37,12 @@ constexpr int kBlock = 256;
 constexpr int kMaxSrcLds = 64;  // source frames per problem
 
 // Mean of the p x p depth block of token (i, j): rows outer, columns inner.
-// P = 2: compile-time 2x2 block; P = 0: runtime p.
+// P = 1 or 2: compile-time block; P = 0: runtime p.
 template <int P>
 __device__ __forceinline__ double pooled(const float* __restrict__ d, int Wd, int i, int j, int p) {
-    if constexpr (P == 2) {
+    if constexpr (P == 1) {
+        return (double)d[(size_t)i * Wd + j];  // pre-pooled map: one value per token
+    } else if constexpr (P == 2) {
         const float2 r0 = *reinterpret_cast<const float2*>(d + (size_t)(2 * i) * Wd + 2 * j);
         const float2 r1 = *reinterpret_cast<const float2*>(d + (size_t)(2 * i + 1) * Wd + 2 * j);
         return ((((double)r0.x + (double)r0.y) + (double)r1.x) + (double)r1.y) * 0.25;  // == / 4
@@ -61,7 +64,8 @@ __device__ __forceinline__ double pooled(const float* __restrict__ d, int Wd, in
 // K / p on the token grid (exact multiply by 0.5 when P = 2).
 template <int P>
 __device__ __forceinline__ double per_token(float k, double pd) {
-    if constexpr (P == 2) return (double)k * 0.5;
+    if constexpr (P == 1) return (double)k;  // == k / 1
+    else if constexpr (P == 2) return (double)k * 0.5;
     else return (double)k / pd;
 }
 
@@ -155,7 +159,7 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const int tok_c = tok < hw ? tok : hw - 1;  // threads past the frame compute a valid token, store nothing
     const int i = tok_c / a.w;
     const int j = tok_c - i * a.w;
-    const int p = P == 2 ? 2 : a.p;
+    const int p = P > 0 ? P : a.p;
     const int Wd = a.w * p;
     const size_t frame_px = (size_t)hw * p * p;
     const int Lq = a.Tq * hw;
@@ -208,6 +212,8 @@ hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream) {
     const dim3 grid(xcd_grid((unsigned)blocks)), block(kBlock);
     if (a.p == 2) {
         hipLaunchKernelGGL(reproject_kernel<2>, grid, block, 0, stream, a);
+    } else if (a.p == 1) {
+        hipLaunchKernelGGL(reproject_kernel<1>, grid, block, 0, stream, a);
     } else {
         hipLaunchKernelGGL(reproject_kernel<0>, grid, block, 0, stream, a);
     }

@@ -191,3 +191,12 @@ def test_stream_null_arguments(L):
     assert L.rc_stream_step(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NULL, NULL) == 1
     assert L.rc_stream_view(None, None) == 1
     assert L.rc_stream_destroy(None) == 0
+
+
+@pytest.mark.parametrize("args,status", [
+    ((FAKE, -1, 30, 52, 2, FAKE), 2), ((FAKE, 3, 0, 52, 2, FAKE), 2), ((FAKE, 3, 30, 52, 0, FAKE), 2),
+    ((NULL, 3, 30, 52, 2, FAKE), 1), ((FAKE, 3, 30, 52, 2, NULL), 1), ((ctypes.c_void_p(0x1002), 3, 30, 52, 2, FAKE), 2),
+    ((NULL, 0, 30, 52, 2, NULL), 0),
+])
+def test_pool_token_depth_rejects(L, args, status):
+    assert L.pool_token_depth(*args, NULL) == status

@@ -211,6 +211,44 @@ def test_reprojection_batched_and_no_source():
     assert (gidx[0, 2] == -5).all() and (gidx[1, 1] == -5).all() and (gidx[1, 3] == -5).all()
 
 
+def test_pooled_depth_and_reprojection_on_pooled_maps():
+    """pool_token_depth bit-exact against the oracle's pooling rounded to fp32
+    (NaN, inf, zero and negative pixels included); reprojection with p = 1 on
+    pooled maps and token-grid intrinsics bit-exact against the oracle on the
+    same maps; and, on maps whose 2 x 2 blocks are constant (exact pooling),
+    bit-identical to the full-resolution call with p = 2."""
+    arrs = W.make_reproj_batch(4, distinct=2)
+    tgt_d, tgt_c, tgt_k, src_d, src_c, src_k = arrs
+    B, Tq, Hd, Wd = tgt_d.shape
+    S = src_d.shape[1]
+    noisy = tgt_d.copy()
+    noisy[0, 0, :4, :4] = [[np.nan, 1.0, 0.0, -2.0], [np.inf, 3.0, 5.0, 5.0], [1e-30, 1e30, 7.0, 7.0], [2.0, 2.0, 7.0, 7.0]]
+    pooled = host(rv.pool_token_depth(dev(noisy.reshape(-1, Hd, Wd)), 2)).reshape(B, Tq, Hd // 2, Wd // 2)
+    want = OR.pooled_depth(noisy, 2).astype(np.float32)
+    assert np.array_equal(np.isnan(pooled), np.isnan(want))
+    ok = ~np.isnan(want)
+    assert np.array_equal(pooled[ok].view(np.uint32), want[ok].view(np.uint32))
+    # p = 1 on pooled maps against the oracle on the same maps
+    ptgt = OR.pooled_depth(tgt_d, 2).astype(np.float32)
+    psrc = OR.pooled_depth(src_d, 2).astype(np.float32)
+    ktok_t = (tgt_k.astype(np.float64) / 2).astype(np.float32)
+    ktok_s = (src_k.astype(np.float64) / 2).astype(np.float32)
+    guv, gidx = rv.reproject_correspondence(dev(ptgt), dev(tgt_c), dev(ktok_t), dev(psrc), dev(src_c), dev(ktok_s),
+                                            p=1, eps=0.05)
+    guv, gidx = host(guv), host(gidx)
+    for b in range(B):
+        ouv, oidx = OR.reproject(ptgt[b], tgt_c[b], ktok_t[b], psrc[b], src_c[b], ktok_s[b], 1, 0.05)
+        _compare_reprojection(ouv, oidx, guv[b], gidx[b], 1, 30, 52, f"pooled {b}")
+    # exactly poolable maps: the pooled call equals the full-resolution call bit for bit
+    blk_t = np.repeat(np.repeat(ptgt, 2, axis=2), 2, axis=3)
+    blk_s = np.repeat(np.repeat(psrc, 2, axis=2), 2, axis=3)
+    fuv, fidx = rv.reproject_correspondence(dev(blk_t), dev(tgt_c), dev(tgt_k), dev(blk_s), dev(src_c), dev(src_k),
+                                            p=2, eps=0.05)
+    assert np.array_equal(host(fidx), gidx)
+    assert np.array_equal(host(fuv).view(np.uint32), guv.view(np.uint32))
+    assert S == 6 and (gidx >= 0).mean() > 0.4
+
+
 def test_reprojection_rejection_codes():
     h, w, p = 6, 8, 2
     Kk = np.array([[8.0, 6.0, 8.0, 6.0]], np.float32)
