@@ -120,10 +120,11 @@ const char* rc_last_error(void);
  * n_bank == 0 or n_query == 0 is valid (count 0 / nothing to do).
  * n_bank <= 2^30; bank_c2w must be 8-byte aligned (REVISIT_ERR_SHAPE
  * otherwise). Banks of more than 8192 entries are scanned by many waves
- * (segments of 1024 entries) whose k best candidates are merged in the same
- * (score, index) order, with the same result; the candidates go to the
- * library-owned per-stream workspace described at biased_chunk_attention
- * (n_query * segments * k * 12 bytes).
+ * (workgroups of 16 waves over segments of 16384 entries) whose k best
+ * candidates are merged in the same (score, index) order, with the same
+ * result; the segments' candidates go to the library-owned per-stream
+ * workspace described at biased_chunk_attention (n_query * segments * k * 12
+ * bytes).
  */
 int retrieve_chunks(const float* bank_c2w, int32_t n_bank,
                     const float* query_c2w, const int32_t* query_chunk, int32_t n_query,

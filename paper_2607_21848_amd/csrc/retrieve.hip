@@ -11,9 +11,10 @@
 // reproducible bit for bit on the host.
 //
 // Large banks (more than kDirectMax entries) are cut into segments of
-// kSegEntries, one wave per (query, segment), so that enough waves stream
-// the bank to keep HBM busy; each leaves its k best (score, j) pairs in a
-// workspace, and one workgroup per query merges them in the same order. The
+// kSegEntries, one workgroup of kSegWaves waves per (query, segment), so that
+// enough waves stream the bank to keep HBM busy; each workgroup merges its
+// waves' lists in LDS and leaves the segment's k best (score, j) pairs in a
+// workspace, and one workgroup per query merges those in the same order. The
 // result is the same as the single-wave scan.
 
 #include <hip/hip_runtime.h>
@@ -28,8 +29,10 @@ namespace revisit {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kSegEntries = 16 * kWave;  // bank entries per segment wave (64 KiB of poses)
-constexpr int kDirectMax = 8192;          // larger banks take the segmented path
+constexpr int kWaveEntries = 16 * kWave;                // bank entries per scanning wave (64 KiB of poses)
+constexpr int kSegWaves = 16;                           // scanning waves per segment workgroup
+constexpr int kSegEntries = kSegWaves * kWaveEntries;   // bank entries per segment
+constexpr int kDirectMax = 8192;                        // larger banks take the segmented path
 
 // (s1, j1) strictly before (s2, j2): smaller score, then smaller index.
 __device__ __forceinline__ bool before(double s1, int j1, double s2, int j2) {
@@ -196,26 +199,53 @@ __global__ __launch_bounds__(kWave) void retrieve_kernel(RetrieveArgs a) {
     emit(a, qi, lane, top);
 }
 
-// Segment `seg` of the bank for query qi: the wave's k best pairs go to
-// seg_s / seg_j [qi][seg][0 .. k), (INFINITY, INT32_MAX) past the admissible ones.
+// Segment `seg` of the bank for query qi, one workgroup of kSegWaves waves:
+// each wave scans kWaveEntries entries and reduces its lanes' lists to its k
+// best pairs in LDS; the first wave merges those and writes the segment's k
+// best to seg_s / seg_j [qi][seg][0 .. k), (INFINITY, INT32_MAX) past the
+// admissible ones.
 template <int KMAX>
-__global__ __launch_bounds__(kWave) void retrieve_segment_kernel(RetrieveArgs a) {
+__global__ __launch_bounds__(kSegWaves * kWave) void retrieve_segment_kernel(RetrieveArgs a) {
+    __shared__ double lds_s[kSegWaves][KMAX];
+    __shared__ int lds_j[kSegWaves][KMAX];
     const int qi = blockIdx.x / a.n_seg;
     const int seg = blockIdx.x - qi * a.n_seg;
-    const int lane = threadIdx.x;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
     const QueryPose qp = query_pose(a, qi);
     LaneTop<KMAX> top;
     top.clear();
-    const int j_end = (int)min((int64_t)a.n_bank, (int64_t)(seg + 1) * kSegEntries);
-    scan_range(a, seg * kSegEntries, j_end, lane, qp, top);
-    const size_t base = ((size_t)qi * a.n_seg + seg) * a.k;
+    const int64_t j0 = (int64_t)seg * kSegEntries + (int64_t)wave * kWaveEntries;
+    const int j_begin = (int)min((int64_t)a.n_bank, j0);
+    const int j_end = (int)min((int64_t)a.n_bank, j0 + kWaveEntries);
+    scan_range(a, j_begin, j_end, lane, qp, top);
     for (int r = 0; r < a.k; ++r) {
         double bs;
         int bj;
         top.wave_best(bs, bj);
         if (lane == 0) {
-            a.seg_s[base + r] = bs;
-            a.seg_j[base + r] = bj;
+            lds_s[wave][r] = bs;
+            lds_j[wave][r] = bj;
+        }
+    }
+    __syncthreads();
+    if (wave == 0) {
+        LaneTop<KMAX> top2;
+        top2.clear();
+        for (int c = lane; c < kSegWaves * a.k; c += kWave) {
+            const int w = c / a.k, r = c - w * a.k;
+            if (lds_j[w][r] != INT32_MAX) top2.offer(lds_s[w][r], lds_j[w][r]);
+        }
+        const size_t base = ((size_t)qi * a.n_seg + seg) * a.k;
+        for (int r = 0; r < a.k; ++r) {
+            double bs;
+            int bj;
+            top2.wave_best(bs, bj);
+            if (lane == 0) {
+                a.seg_s[base + r] = bs;
+                a.seg_j[base + r] = bj;
+            }
         }
     }
 }
@@ -281,7 +311,8 @@ static hipError_t launch_k(const RetrieveArgs& a, hipStream_t stream) {
         hipLaunchKernelGGL(retrieve_kernel<KMAX>, dim3(a.n_query), block, 0, stream, a);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(retrieve_segment_kernel<KMAX>, dim3((unsigned)a.n_query * a.n_seg), block, 0, stream, a);
+    hipLaunchKernelGGL(retrieve_segment_kernel<KMAX>, dim3((unsigned)a.n_query * a.n_seg), dim3(kSegWaves * kWave), 0,
+                       stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(retrieve_merge_kernel<KMAX>, dim3(a.n_query), dim3(kMergeThreads), 0, stream, a);
