@@ -66,8 +66,11 @@ enum {
     REVISIT_ERR_MEMORY = 6       /* a stream object could not get its memory */
 };
 
-/* Element types of biased_chunk_attention. */
-enum { REVISIT_BF16 = 1, REVISIT_F32 = 2 };
+/* Element types of biased_chunk_attention (and of the other calls where they
+ * apply). REVISIT_FP8_QK: q and k in fp8 e4m3 (OCP: 1 sign, 4 exponent bits
+ * with bias 7, 3 mantissa bits, no infinities, 0x7f / 0xff NaN), v and o in
+ * bf16. */
+enum { REVISIT_BF16 = 1, REVISIT_F32 = 2, REVISIT_FP8_QK = 3 };
 
 /* Correspondence reason codes written to out_idx by reproject_correspondence
  * (the rejection causes of Sec. 4.3, design choice (iii), plus an empty
@@ -188,9 +191,12 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
  * with (k_y, k_x) = divmod(k mod (h w), w). The bias is computed on the fly
  * from the correspondence map, never materialised.
  *
- *   dtype       REVISIT_BF16 (D = 128) or REVISIT_F32 (D = 64 or 128)
+ *   dtype       REVISIT_BF16 (D = 128), REVISIT_F32 (D = 64 or 128) or
+ *               REVISIT_FP8_QK (D = 128: q, k fp8 e4m3, v, o bf16; the
+ *               logits come from the fp8 matrix cores, so any dequantisation
+ *               scales of q and k belong in softmax_scale)
  *   q           [Lq][H][D], k, v [Lk][H][D], o [Lq][H][D] in dtype
- *               (fp32 accumulation and softmax in both cases)
+ *               (fp32 accumulation and softmax in every case)
  *   lse         nullable [H][Lq] fp32
  *   Lq >= 0, Lk >= 1, Lk % (h*w) == 0, Lk / (h*w) <= 1024 KV frames
  *   kv_frame_slot [Lk/(h*w)] int32: s in [0, S) for a retrieved frame, any

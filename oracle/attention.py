@@ -32,6 +32,18 @@ from __future__ import annotations
 import numpy as np
 
 
+def fp8e4m3_values(bits: np.ndarray) -> np.ndarray:
+    """Exact float64 values of fp8 e4m3 codes (OCP: sign, 4 exponent bits with
+    bias 7, 3 mantissa bits; exponent 0 subnormal; 0x7f / 0xff NaN)."""
+    b = np.asarray(bits, dtype=np.uint8).astype(np.int64)
+    sign = np.where(b & 0x80, -1.0, 1.0)
+    e = (b >> 3) & 0xF
+    m = (b & 0x7).astype(np.float64)
+    mag = np.where(e == 0, np.ldexp(m / 8.0, -6), np.ldexp(1.0 + m / 8.0, e - 7))
+    mag = np.where((e == 15) & (m == 7), np.nan, mag)
+    return sign * mag
+
+
 def key_centres(Lk, h, w):
     """Token-grid centres (x, y) of every key column: [Lk, 2] float64."""
     t = np.arange(Lk) % (h * w)

@@ -23,7 +23,7 @@ from typing import Optional, Sequence
 import torch
 
 from . import _lib
-from ._lib import BF16, F32, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
+from ._lib import BF16, F32, FP8_QK, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
 
 __all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "pack_retrieved_kv",
            "pool_token_depth", "StreamDriver", "set_attention_key_parts",
@@ -140,7 +140,8 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
                            return_lse: bool = True, out=None):
     """Attention with the Gaussian correspondence bias on retrieved-frame keys.
 
-    q [Lq,H,D], k, v [Lk,H,D] (bf16 with D=128, or fp32 with D in {64,128});
+    q [Lq,H,D], k, v [Lk,H,D] (bf16 with D=128, or fp32 with D in {64,128}, or
+    q, k float8_e4m3fn with v bf16 and D=128: fp8 logits, o bf16);
     kv_frame_slot [Lk/(h*w)] i32; corr_uv [S,Lq,2] f32 and corr_idx [S,Lq] i32
     (None = no bias). Returns (o [Lq,H,D], lse [H,Lq] f32 or None)."""
     dev = q.device
@@ -150,11 +151,14 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
         dt = BF16
     elif q.dtype == torch.float32:
         dt = F32
+    elif q.dtype == torch.float8_e4m3fn:
+        dt = FP8_QK
     else:
-        raise TypeError(f"q must be bfloat16 or float32 (got {q.dtype})")
+        raise TypeError(f"q must be bfloat16, float32 or float8_e4m3fn (got {q.dtype})")
+    vdt = torch.bfloat16 if dt == FP8_QK else q.dtype  # fp8 q, k come with bf16 v, o
     _need(q, "q", q.dtype, None, dev)
     _need(k, "k", q.dtype, (Lk, H, D), dev)
-    _need(v, "v", q.dtype, (Lk, H, D), dev)
+    _need(v, "v", vdt, (Lk, H, D), dev)
     _need(kv_frame_slot, "kv_frame_slot", torch.int32, None, dev)
     S = 0
     if corr_uv is not None:
@@ -162,11 +166,11 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
         _need(corr_uv, "corr_uv", torch.float32, (S, Lq, 2), dev)
         _need(corr_idx, "corr_idx", torch.int32, (S, Lq), dev)
     if out is None:
-        o = torch.empty_like(q)
+        o = torch.empty((Lq, H, D), dtype=vdt, device=dev)
         lse = torch.empty((H, Lq), dtype=torch.float32, device=dev) if return_lse else None
     else:
         o, lse = out
-        _need(o, "o", q.dtype, (Lq, H, D), dev)
+        _need(o, "o", vdt, (Lq, H, D), dev)
         if lse is not None:
             _need(lse, "lse", torch.float32, (H, Lq), dev)
     st = lib().biased_chunk_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), dt, Lq, Lk, H, D, h, w,

@@ -14,7 +14,7 @@ _LIB = None
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librevisit.so")
 
 OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH, ERR_MEMORY = 0, 1, 2, 3, 4, 5, 6
-BF16, F32 = 1, 2
+BF16, F32, FP8_QK = 1, 2, 3
 MAX_K = 32
 EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
             "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv", "pool_token_depth", "rc_stream_create",

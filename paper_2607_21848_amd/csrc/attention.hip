@@ -274,6 +274,19 @@ struct KeySplit {
 constexpr int kPartFloats = 128 * kD + 2 * 128;  // O [128 queries][kD], then m [128], l [128]
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef int int8v __attribute__((ext_vector_type(8)));
+
+// 32 fp8 operand bytes from two 16-byte reads
+__device__ __forceinline__ int8v join8(u32x4 a, u32x4 b) {
+    return int8v{(int)a[0], (int)a[1], (int)a[2], (int)a[3], (int)b[0], (int)b[1], (int)b[2], (int)b[3]};
+}
+// D += A B on the fp8 matrix cores, A and B e4m3 (format code 0), no block
+// scaling: lane l supplies row / column l % 32 and contraction indices
+// 32 (l / 32) .. + 32, and D comes back in the same 32 x 32 accumulator layout
+// as v_mfma_f32_32x32x16_bf16 (both checked on the device)
+__device__ __forceinline__ floatx16 mfma_fp8(int8v a, int8v b, floatx16 c) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -326,30 +339,47 @@ __device__ __forceinline__ float half_swap_sum(float x) {
     return __uint_as_float(p[0]) + __uint_as_float(p[1]);
 }
 
-// Direct global -> LDS loads of one K or V tile. Wave `wave` fills its
-// quarter of the tile with 1 KB instructions (64 lanes x 16 bytes). Lane byte offsets relative to the tile's first row
-// are fixed for the whole kernel (`off`); only the uniform base moves. On the
-// last tile, rows past Lk are redirected to the last valid row (their logits
-// are masked), so no load leaves the tensor.
-constexpr int kLoadsPerLane = kTileBytes / (256 * 16);  // 16-byte direct loads per lane per tile
+// Direct global -> LDS loads of one K or V tile of 32 rows. Wave `wave`
+// fills its quarter of the tile with 1 KB instructions (64 lanes x 16
+// bytes). Lane byte offsets relative to the tile's first row are fixed for
+// the whole kernel (`off`); only the uniform base moves. On the last tile,
+// rows past Lk are redirected to the last valid row (their logits are
+// masked), so no load leaves the tensor. Rows are 256 bytes (bf16) or 128
+// bytes (fp8 keys); the 16-byte chunks of row r sit at chunk position
+// c ^ swz(r), a swizzle under which every operand read pattern of the kernel
+// touches distinct bank groups.
+template <int ROW_BYTES>
+struct TileFmt {
+    static constexpr int kChunks = ROW_BYTES / 16;
+    static constexpr int kLoads = kTK * ROW_BYTES / (256 * 16);  // 16-byte direct loads per lane per tile
+    static __device__ __forceinline__ int swizzle(int r) { return ROW_BYTES == 256 ? swz(r) : ((r >> 1) & 7); }
+};
+using RowsBf16 = TileFmt<256>;
+using RowsFp8 = TileFmt<128>;
+constexpr int kLoadsPerLane = RowsBf16::kLoads;  // V tiles (and bf16 K tiles)
 
+template <class Fmt>
 struct TileLoad {
-    uint32_t off[kLoadsPerLane];  // byte offset of this lane's chunk from the tile's first row
+    uint32_t off[Fmt::kLoads];  // byte offset of this lane's chunk from the tile's first row
 };
 
+template <class Fmt>
 __device__ __forceinline__ void tile_chunk(int wave, int lane, int i, int& r, int& lc) {
-    const int pos = (wave * kLoadsPerLane + i) * 64 + lane;  // 16-byte chunk position in the tile
-    r = pos >> 4;
-    lc = (pos & 15) ^ swz(r);                    // logical chunk stored at this position
+    const int pos = (wave * Fmt::kLoads + i) * 64 + lane;  // 16-byte chunk position in the tile
+    r = pos / Fmt::kChunks;
+    lc = (pos % Fmt::kChunks) ^ Fmt::swizzle(r);  // logical chunk stored at this position
 }
 
-__device__ __forceinline__ TileLoad make_tile_load(size_t row_stride, int hd, int wave, int lane) {
-    TileLoad t;
+// row_bytes: bytes between consecutive tokens in global memory; head hd's
+// row starts hd * ROW_BYTES into it
+template <class Fmt>
+__device__ __forceinline__ TileLoad<Fmt> make_tile_load(size_t row_bytes, int hd, int wave, int lane) {
+    TileLoad<Fmt> t;
 #pragma unroll
-    for (int i = 0; i < kLoadsPerLane; ++i) {
+    for (int i = 0; i < Fmt::kLoads; ++i) {
         int r, lc;
-        tile_chunk(wave, lane, i, r, lc);
-        t.off[i] = (uint32_t)(r * (int)(row_stride * 2) + (hd * kD + lc * 8) * 2);
+        tile_chunk<Fmt>(wave, lane, i, r, lc);
+        t.off[i] = (uint32_t)(r * (int)row_bytes + hd * (Fmt::kChunks * 16) + lc * 16);
     }
     return t;
 }
@@ -377,20 +407,20 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 }
 
 // lds_wave: LDS byte address of this wave's quarter of the destination tile (uniform)
-__device__ __forceinline__ void load_tile_lds(const uint16_t* __restrict__ src, uint32_t lds_wave, int tile0,
-                                              int Lk, size_t row_stride, const TileLoad& tl, int hd, int wave,
-                                              int lane) {
-    const uint8_t* base = reinterpret_cast<const uint8_t*>(src) + (size_t)tile0 * row_stride * 2;
+template <class Fmt>
+__device__ __forceinline__ void load_tile_lds(const uint8_t* __restrict__ src, uint32_t lds_wave, int tile0, int Lk,
+                                              size_t row_bytes, const TileLoad<Fmt>& tl, int hd, int wave, int lane) {
+    const uint8_t* base = src + (size_t)tile0 * row_bytes;
     if (tile0 + kTK <= Lk) {
 #pragma unroll
-        for (int i = 0; i < kLoadsPerLane; ++i) dma_b128(base, tl.off[i], lds_wave + i * 1024);
+        for (int i = 0; i < Fmt::kLoads; ++i) dma_b128(base, tl.off[i], lds_wave + i * 1024);
     } else {
         const int last = Lk - 1 - tile0;
 #pragma unroll
-        for (int i = 0; i < kLoadsPerLane; ++i) {
+        for (int i = 0; i < Fmt::kLoads; ++i) {
             int r, lc;
-            tile_chunk(wave, lane, i, r, lc);
-            const uint32_t off = (uint32_t)(min(r, last) * (int)(row_stride * 2) + (hd * kD + lc * 8) * 2);
+            tile_chunk<Fmt>(wave, lane, i, r, lc);
+            const uint32_t off = (uint32_t)(min(r, last) * (int)row_bytes + hd * (Fmt::kChunks * 16) + lc * 16);
             dma_b128(base, off, lds_wave + i * 1024);
         }
     }
@@ -408,7 +438,9 @@ __device__ __forceinline__ void wg_barrier() {
 }
 
 
-template <bool kBias>
+// kFp8: q and k hold fp8 e4m3 values and Q K^T runs on the fp8 matrix cores
+// (v_mfma_f32_32x32x64_f8f6f4, two per 32-key tile); v, o and P V stay bf16.
+template <bool kBias, bool kFp8>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, BiasGeom g, float c_log2, KeySplit ks) {
     // Three-slot ring: slot t mod 3 holds K_t in its first half and V_{t-1}
     // in its second. Step j refills slot j mod 3 (K_{j+3}, V_{j+2}) while it
@@ -449,22 +481,33 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     const int t0 = (int)((int64_t)kp * n_tiles / ks.parts);
     const int nt = (int)((int64_t)(kp + 1) * n_tiles / ks.parts) - t0;
     const int H = a.H;
-    const uint16_t* Qg = static_cast<const uint16_t*>(a.q);
-    const uint16_t* Kg = static_cast<const uint16_t*>(a.k);
-    const uint16_t* Vg = static_cast<const uint16_t*>(a.v);
-    const size_t row_stride = (size_t)H * kD;  // elements between consecutive tokens
+    using KFmt = std::conditional_t<kFp8, RowsFp8, RowsBf16>;
+    const uint8_t* Qg = static_cast<const uint8_t*>(a.q);
+    const uint8_t* Kg = static_cast<const uint8_t*>(a.k);
+    const uint8_t* Vg = static_cast<const uint8_t*>(a.v);
+    const size_t row_stride = (size_t)H * kD;              // elements between consecutive tokens (o)
+    const size_t qk_row_bytes = row_stride * (kFp8 ? 1 : 2);
+    const size_t v_row_bytes = row_stride * 2;
     using R0 = std::integral_constant<int, 0>;
     using R1 = std::integral_constant<int, 1>;
     using R2 = std::integral_constant<int, 2>;
-    // this wave's quarter of a K tile in each ring slot (+ kTileBytes: the V tile)
-    const uint32_t wave_off = (uint32_t)__builtin_amdgcn_readfirstlane(wave * kLoadsPerLane * 1024);
-    auto dst = [&](auto slot_tag) -> uint32_t { return lds_addr(ring(slot_tag)) + wave_off; };
+    // this wave's quarter of the K tile of a ring slot, and of its V tile (kTileBytes further)
+    const uint32_t wave_off_k = (uint32_t)__builtin_amdgcn_readfirstlane(wave * KFmt::kLoads * 1024);
+    const uint32_t wave_off_v = (uint32_t)__builtin_amdgcn_readfirstlane(wave * kLoadsPerLane * 1024);
+    auto kdst = [&](auto slot_tag) -> uint32_t { return lds_addr(ring(slot_tag)) + wave_off_k; };
+    auto vdst = [&](auto slot_tag) -> uint32_t { return lds_addr(ring(slot_tag)) + kTileBytes + wave_off_v; };
 
     // LDS byte offsets (within a tile) of this lane's operand reads
     const int krow = perm_row(n);
-    int koff[8];
+    // bf16: eight 16-byte reads per tile, kk -> d 16 kk + 8 hh ..; fp8: two 32-byte
+    // operands per tile, kk -> d 64 kk + 32 hh .., each two 16-byte reads
+    constexpr int kKReads = kFp8 ? 4 : 8;
+    int koff[kKReads];
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) koff[kk] = krow * kRowBytes + (((2 * kk + hh) ^ swz(krow)) << 4);
+    for (int i = 0; i < kKReads; ++i) {
+        if constexpr (kFp8) koff[i] = krow * 128 + (((4 * (i >> 1) + 2 * hh + (i & 1)) ^ RowsFp8::swizzle(krow)) << 4);
+        else koff[i] = krow * kRowBytes + (((2 * i + hh) ^ swz(krow)) << 4);
+    }
     // V transpose reads: lane t of 16-lane group G reads row 8 hh + t / 4 (+4 for the
     // second half) at columns 32 db + 16 (G % 2) + 4 (t % 4) .. +3
     const int t16 = lane & 15;
@@ -511,21 +554,35 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // part, everything its first step expects in place. With fewer tiles the missing
     // ones repeat the last tile (never read; loading them anyway keeps these
     // loads free of branches).
-    const TileLoad tl = make_tile_load(row_stride, hd, wave, lane);
+    const TileLoad<KFmt> tlk = make_tile_load<KFmt>(qk_row_bytes, hd, wave, lane);
+    const TileLoad<RowsBf16> tlv = make_tile_load<RowsBf16>(v_row_bytes, hd, wave, lane);
     const int tile0 = t0 * kTK, tile1 = (t0 + min(1, nt - 1)) * kTK, tile2 = (t0 + min(2, nt - 1)) * kTK;
-    load_tile_lds(Kg, dst(R0{}), tile0, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Vg, dst(R1{}) + kTileBytes, tile0, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Kg, dst(R1{}), tile1, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Vg, dst(R2{}) + kTileBytes, tile1, Lk, row_stride, tl, hd, wave, lane);
-    load_tile_lds(Kg, dst(R2{}), tile2, Lk, row_stride, tl, hd, wave, lane);
+    load_tile_lds(Kg, kdst(R0{}), tile0, Lk, qk_row_bytes, tlk, hd, wave, lane);
+    load_tile_lds(Vg, vdst(R1{}), tile0, Lk, v_row_bytes, tlv, hd, wave, lane);
+    load_tile_lds(Kg, kdst(R1{}), tile1, Lk, qk_row_bytes, tlk, hd, wave, lane);
+    load_tile_lds(Vg, vdst(R2{}), tile1, Lk, v_row_bytes, tlv, hd, wave, lane);
+    load_tile_lds(Kg, kdst(R2{}), tile2, Lk, qk_row_bytes, tlk, hd, wave, lane);
 
     // Q fragments: lane (hh, n) holds Q[q][16 kk + 8 hh .. +8)
-    bf16x8 qf[8];
+    // (fp8: lane (hh, n) holds Q[q][64 kk + 32 hh .. +32), kk = 0, 1)
+    constexpr int kQFrags = kFp8 ? 2 : 8;
+    using QFrag = std::conditional_t<kFp8, int8v, bf16x8>;
+    QFrag qf[kQFrags];
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-        u32x4 v = u32x4{0, 0, 0, 0};
-        if (q_ok) v = *reinterpret_cast<const u32x4*>(Qg + (size_t)q * row_stride + (size_t)hd * kD + 16 * kk + 8 * hh);
-        qf[kk] = as_bf16x8(v);
+    for (int kk = 0; kk < kQFrags; ++kk) {
+        if constexpr (kFp8) {
+            u32x4 v0 = u32x4{0, 0, 0, 0}, v1 = u32x4{0, 0, 0, 0};
+            if (q_ok) {
+                const uint8_t* qp = Qg + (size_t)q * qk_row_bytes + (size_t)hd * kD + 64 * kk + 32 * hh;
+                v0 = *reinterpret_cast<const u32x4*>(qp);
+                v1 = *reinterpret_cast<const u32x4*>(qp + 16);
+            }
+            qf[kk] = int8v{(int)v0[0], (int)v0[1], (int)v0[2], (int)v0[3], (int)v1[0], (int)v1[1], (int)v1[2], (int)v1[3]};
+        } else {
+            u32x4 v = u32x4{0, 0, 0, 0};
+            if (q_ok) v = *reinterpret_cast<const u32x4*>(Qg + ((size_t)q * row_stride + (size_t)hd * kD + 16 * kk + 8 * hh) * 2);
+            qf[kk] = as_bf16x8(v);
+        }
     }
 
     // Correspondences of the 128 queries for the first kCorrLds
@@ -633,9 +690,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             S = floatx16{0};
         }
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
-            const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(kt + koff[kk]));
-            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], S, 0, 0, 0);
+        for (int kk = 0; kk < kQFrags; ++kk) {
+            if constexpr (kFp8) {
+                const u32x4 k0 = *reinterpret_cast<const u32x4*>(kt + koff[2 * kk]);
+                const u32x4 k1 = *reinterpret_cast<const u32x4*>(kt + koff[2 * kk + 1]);
+                S = mfma_fp8(join8(k0, k1), qf[kk], S);
+            } else {
+                const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(kt + koff[kk]));
+                S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], S, 0, 0, 0);
+            }
         }
     };
     // mask keys past Lk (only the last tile can hold any) and reduce this lane's maximum
@@ -673,7 +736,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // Loads issued in step j - 1 may stay in flight: each lane waits only for
     // those of step j - 2, which carried K_{j+1} and V_j.
     // The body takes the ring slots (knext: the slot holding K_{j+1} and V_j;
-    // refill: this wave's part of slot j mod 3) and the logit buffers as
+    // refill: the LDS address of slot j mod 3) and the logit buffers as
     // arguments: compile-time in the steady loop, chosen at run time in the
     // last few steps.
     auto step_core = [&](auto kind_tag, int j, floatx16& S_cur, floatx16& S_next, const uint8_t* knext,
@@ -683,20 +746,21 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         const uint8_t* vcur = knext + kTileBytes;
         // this lane's loads issued in step j - 1: K_{j+2} if it exists, V_{j+1} if it exists
         if constexpr (kind <= 1) {
-            __builtin_amdgcn_s_waitcnt(kWaitVm0 + 2 * kLoadsPerLane);
+            __builtin_amdgcn_s_waitcnt(kWaitVm0 + KFmt::kLoads + kLoadsPerLane);
         } else if constexpr (kind == 2) {
             __builtin_amdgcn_s_waitcnt(kWaitVm0 + kLoadsPerLane);
         } else {
             __builtin_amdgcn_s_waitcnt(kWaitVm0);
         }
         wg_barrier();
-        if constexpr (kind == 0) load_tile_lds(Kg, refill, (t0 + j + 3) * kTK, Lk, row_stride, tl, hd, wave, lane);
-        if constexpr (kind <= 1) load_tile_lds(Vg, refill + kTileBytes, (t0 + j + 2) * kTK, Lk, row_stride, tl, hd, wave, lane);
+        if constexpr (kind == 0) load_tile_lds(Kg, refill + wave_off_k, (t0 + j + 3) * kTK, Lk, qk_row_bytes, tlk, hd, wave, lane);
+        if constexpr (kind <= 1)
+            load_tile_lds(Vg, refill + kTileBytes + wave_off_v, (t0 + j + 2) * kTK, Lk, v_row_bytes, tlv, hd, wave, lane);
 
         // K_{j+1} operands of the first QK MFMAs, read while the rescale check runs
         const int nk0 = (t0 + j + 1) * kTK;
-        auto kread = [&](int kk) -> bf16x8 { return as_bf16x8(*reinterpret_cast<const u32x4*>(knext + koff[kk])); };
-        bf16x8 kf[8];
+        auto kread = [&](int i) -> u32x4 { return *reinterpret_cast<const u32x4*>(knext + koff[i]); };
+        u32x4 kf[kKReads];
         if constexpr (has_next) {
             kf[0] = kread(0);
             kf[1] = kread(1);
@@ -751,17 +815,36 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         };
         __builtin_amdgcn_sched_barrier(0);
 
-        // region A: the 8 QK MFMAs of tile j + 1 (K operands read three ahead),
-        // softmax units (0, 0..3) and (1, 0..1), V reads of key half 0
+        if constexpr (kFp8) {
+            // region A: the 2 fp8 QK MFMAs of tile j + 1 (64 cycles each), each
+            // carrying three softmax units; the second also the V reads of key half 0
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
-            if constexpr (has_next) {
-                if (kk + 3 < 8) kf[kk + 3] = kread(kk + 3);
-                S_next = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], S_next, 0, 0, 0);
+            for (int kk = 0; kk < 2; ++kk) {
+                if constexpr (has_next) {
+                    if (kk == 0) kf[3] = kread(3);
+                    S_next = mfma_fp8(join8(kf[2 * kk], kf[2 * kk + 1]), qf[kk], S_next);
+                }
+#pragma unroll
+                for (int u = 3 * kk; u < 3 * kk + 3; ++u) unit(u >> 2, u & 3);
+                if (kk == 1) {
+#pragma unroll
+                    for (int db = 0; db < 4; ++db) vread(0, db);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
-            if (kk < 6) unit(kk >> 2, kk & 3);
-            if (kk >= 4) vread(0, kk - 4);
-            __builtin_amdgcn_sched_barrier(0);
+        } else {
+            // region A: the 8 QK MFMAs of tile j + 1 (K operands read three ahead),
+            // softmax units (0, 0..3) and (1, 0..1), V reads of key half 0
+#pragma unroll
+            for (int kk = 0; kk < 8; ++kk) {
+                if constexpr (has_next) {
+                    if (kk + 3 < 8) kf[kk + 3] = kread(kk + 3);
+                    S_next = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[kk]), qf[kk], S_next, 0, 0, 0);
+                }
+                if (kk < 6) unit(kk >> 2, kk & 3);
+                if (kk >= 4) vread(0, kk - 4);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
         const bf16x8 pf0 = as_bf16x8(u32x4{w4[0][0], w4[0][1], w4[0][2], w4[0][3]});
 
@@ -798,7 +881,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     auto step = [&](auto phase_tag, auto kind_tag, int j) __attribute__((always_inline)) {
         constexpr int P = decltype(phase_tag)::value;
         step_core(kind_tag, j, (P & 1) ? Sb : Sa, (P & 1) ? Sa : Sb, ring(std::integral_constant<int, P + 1>{}),
-                  dst(std::integral_constant<int, P>{}));
+                  lds_addr(ring(std::integral_constant<int, P>{})));
     };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
@@ -832,7 +915,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     int slot = 0;
     auto tail_step = [&](auto kind_tag) __attribute__((always_inline)) {
         const int nxt = slot == 2 ? 0 : slot + 1;
-        step_core(kind_tag, j, Sa, Sb, slot_base(nxt), lds_addr(slot_base(slot)) + wave_off);
+        step_core(kind_tag, j, Sa, Sb, slot_base(nxt), lds_addr(slot_base(slot)));
         if constexpr (decltype(kind_tag)::value != 3) Sa = Sb;
         slot = nxt;
         ++j;
@@ -979,10 +1062,13 @@ hipError_t launch_attention_bf16(const AttentionArgs& a, int32_t parts, float* w
     const unsigned items = (unsigned)(((a.Lq + 127) / 128) * a.H);
     const KeySplit ks{parts, workspace};
     const dim3 grid(xcd_grid(items * (unsigned)parts)), block(256);
-    if (bias_on) {
-        hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e, ks);
+    const float c_log2 = a.softmax_scale * kLog2e;
+    if (a.fp8_qk) {
+        if (bias_on) hipLaunchKernelGGL((attn_bf16_kernel<true, true>), grid, block, 0, stream, a, g, c_log2, ks);
+        else hipLaunchKernelGGL((attn_bf16_kernel<false, true>), grid, block, 0, stream, a, g, c_log2, ks);
     } else {
-        hipLaunchKernelGGL(attn_bf16_kernel<false>, grid, block, 0, stream, a, g, a.softmax_scale * kLog2e, ks);
+        if (bias_on) hipLaunchKernelGGL((attn_bf16_kernel<true, false>), grid, block, 0, stream, a, g, c_log2, ks);
+        else hipLaunchKernelGGL((attn_bf16_kernel<false, false>), grid, block, 0, stream, a, g, c_log2, ks);
     }
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && parts > 1) {

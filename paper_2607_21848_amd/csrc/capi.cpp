@@ -168,10 +168,10 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
                            int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
                            const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx, int32_t S,
                            float softmax_scale, float lambda, float sigma, hipStream_t stream) {
-    if (dtype != REVISIT_BF16 && dtype != REVISIT_F32)
+    if (dtype != REVISIT_BF16 && dtype != REVISIT_F32 && dtype != REVISIT_FP8_QK)
         return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: dtype %d not supported", dtype);
-    if (dtype == REVISIT_BF16 && D != 128)
-        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: bf16 needs D = 128 (got %d)", D);
+    if ((dtype == REVISIT_BF16 || dtype == REVISIT_FP8_QK) && D != 128)
+        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: bf16 / fp8 needs D = 128 (got %d)", D);
     if (dtype == REVISIT_F32 && D != 64 && D != 128)
         return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: fp32 needs D = 64 or 128 (got %d)", D);
     if (Lq < 0 || Lk < 1 || H < 1 || h < 1 || w < 1 || S < 0)
@@ -219,6 +219,7 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     a.softmax_scale = softmax_scale;
     a.lambda = lambda;
     a.sigma = sigma;
+    a.fp8_qk = dtype == REVISIT_FP8_QK;
     if (dtype == REVISIT_F32) return launched(revisit::launch_attention_f32(a, stream), "biased_chunk_attention");
     if (Lq == 0) return REVISIT_OK;
     int32_t parts = g_attention_key_parts.load();

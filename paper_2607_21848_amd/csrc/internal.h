@@ -73,6 +73,7 @@ struct AttentionArgs {
     const int32_t* corr_idx;  // [S][Lq]
     int32_t S;  // 0 = bias off
     float softmax_scale, lambda, sigma;
+    int32_t fp8_qk;  // bf16 kernel: q and k are fp8 e4m3 (v, o bf16)
 };
 hipError_t launch_attention_f32(const AttentionArgs& a, hipStream_t stream);
 
@@ -85,8 +86,6 @@ int32_t attention_bf16_key_parts(const AttentionArgs& a, int32_t slots);
 size_t attention_bf16_workspace_bytes(const AttentionArgs& a, int32_t parts);
 hipError_t launch_attention_bf16(const AttentionArgs& a, int32_t parts, float* workspace, hipStream_t stream);
 
-// Library-owned device memory of `bytes` for work queued on `stream` of the
-// current device (see workspace.cpp); compute units of the current device.
 // Cache packing of retrieved chunks (kvpack.hip). Element size 2 (bf16) or
 // 4 (fp32); T = tokens per chunk; store [L][n_store][T][H][D], cache
 // [L][cache_rows][H][D].
@@ -147,10 +146,12 @@ hipError_t launch_stream_slots(const StreamSlotsArgs& a, hipStream_t stream);
 hipError_t launch_pool_depth(const float* depth, int64_t n_tokens, int32_t h, int32_t w, int32_t p, float* out,
                              hipStream_t stream);
 
+// Library-owned device memory of `bytes` for work queued on `stream` of the
+// current device (see workspace.cpp); compute units of the current device.
 hipError_t stream_workspace(hipStream_t stream, size_t bytes, void** out);
+hipError_t device_compute_units(int* cus);
 
 // Sets the calling thread's last-error string and returns status (capi.cpp).
 int fail_status(int status, const char* fmt, ...);
-hipError_t device_compute_units(int* cus);
 
 }  // namespace revisit

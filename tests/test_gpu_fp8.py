@@ -1,0 +1,114 @@
+"""fp8 logits (REVISIT_FP8_QK): q and k in fp8 e4m3, v and o in bf16.
+
+Parity: the oracle runs on the exact values of the fp8 q, k and the bf16 v,
+so the bars of the bf16 path apply (max |dO| <= 2e-2, |dLSE| <= 2e-3). Both
+paths accumulate exact products in fp32; only P is rounded to bf16 for P V.
+Accuracy study (printed, not a gate): the same kernel against the oracle on
+the unquantised bf16 q, k, i.e. what storing q and k in fp8 costs.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_21848_amd as rv
+import workloads as W
+from oracle import attention as OA
+from tests.gpu_helpers import dev, host, sample_rows
+from workloads.synth import fp8e4m3_bits
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL, LSE_BF16_TOL = 2e-2, 2e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rv.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _fp8_dev(codes: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(codes)).cuda().view(torch.float8_e4m3fn)
+
+
+def _case(rng, Lq, Lk, H, h, w, S):
+    D = 128
+    nf = Lk // (h * w)
+    slot = np.full(nf, -1, np.int32)
+    frames = rng.choice(nf, size=min(S, nf), replace=False)
+    slot[frames] = np.arange(len(frames))
+    uv = np.stack([rng.uniform(-1, w + 1, (S, Lq)), rng.uniform(-1, h + 1, (S, Lq))], axis=-1).astype(np.float32)
+    idx = rng.integers(-4, h * w, size=(S, Lq)).astype(np.int32)
+    q32 = rng.standard_normal((Lq, H, D), dtype=np.float32)
+    k32 = rng.standard_normal((Lk, H, D), dtype=np.float32)
+    v = W.bf16_round(rng.standard_normal((Lk, H, D), dtype=np.float32))
+    return fp8e4m3_bits(q32), fp8e4m3_bits(k32), v, slot, uv, idx, W.bf16_round(q32), W.bf16_round(k32)
+
+
+def _run(q8, k8, v, slot, uv, idx, h, w, scale):
+    return rv.biased_chunk_attention(_fp8_dev(q8), _fp8_dev(k8), dev(v, torch.bfloat16), dev(slot), dev(uv), dev(idx),
+                                     h=h, w=w, softmax_scale=scale, lam=1.0, sigma=2.0)
+
+
+@pytest.mark.parametrize("shape", [(1, 20, 1, 4, 5, 2), (100, 60, 2, 3, 4, 3), (129, 300, 3, 6, 5, 4),
+                                   (257, 1560, 2, 30, 52, 1), (300, 4 * 70, 1, 7, 10, 2)])
+def test_fp8_qk_ragged_shapes(shape):
+    Lq, Lk, H, h, w, S = shape
+    rng = np.random.default_rng(Lq * 5 + Lk)
+    q8, k8, v, slot, uv, idx, qb, kb = _case(rng, Lq, Lk, H, h, w, S)
+    scale = 1.0 / math.sqrt(128)
+    o, lse = _run(q8, k8, v, slot, uv, idx, h, w, scale)
+    Oo, Lo = OA.biased_attention(OA.fp8e4m3_values(q8), OA.fp8e4m3_values(k8), v, slot, uv, idx, h, w, scale, 1.0, 2.0)
+    err = np.abs(host(o) - Oo).max()
+    lerr = np.abs(host(lse) - Lo).max()
+    Ob, _ = OA.biased_attention(qb, kb, v, slot, uv, idx, h, w, scale, 1.0, 2.0)
+    print(f"fp8 logits {shape}: max|dO|={err:.3e} max|dLSE|={lerr:.3e}; vs bf16 q, k: max|dO|="
+          f"{np.abs(host(o) - Ob).max():.3e} mean {np.abs(host(o) - Ob).mean():.3e}")
+    assert err <= BF16_TOL and lerr <= LSE_BF16_TOL
+
+
+@pytest.mark.parametrize("parts", [1, 3, 7])
+def test_fp8_qk_key_parts(parts):
+    rng = np.random.default_rng(33)
+    Lq, Lk, H, h, w, S = 300, 40 * 70, 2, 7, 10, 3
+    q8, k8, v, slot, uv, idx, _, _ = _case(rng, Lq, Lk, H, h, w, S)
+    scale = 1.0 / math.sqrt(128)
+    try:
+        rv.set_attention_key_parts(parts)
+        o, lse = _run(q8, k8, v, slot, uv, idx, h, w, scale)
+        torch.cuda.synchronize()
+    finally:
+        rv.set_attention_key_parts(0)
+    Oo, Lo = OA.biased_attention(OA.fp8e4m3_values(q8), OA.fp8e4m3_values(k8), v, slot, uv, idx, h, w, scale, 1.0, 2.0)
+    assert np.abs(host(o) - Oo).max() <= BF16_TOL and np.abs(host(lse) - Lo).max() <= LSE_BF16_TOL
+
+
+def test_fp8_qk_history_bank_shape_sampled():
+    """The Wan-1.3B history-bank shape (H12, Lq 4680, Lk 37440, 12 retrieved
+    frames) with fp8 q, k, at the launch configuration the bench times,
+    checked on sampled query rows."""
+    wl = W.make_config(4, "bf16", qkv=False)
+    rng = np.random.default_rng(404)
+    Lq, Lk, H, D = wl.Lq, wl.Lk, wl.H, wl.D
+    q8 = fp8e4m3_bits(rng.standard_normal((Lq, H, D), dtype=np.float32))
+    k8 = fp8e4m3_bits(rng.standard_normal((Lk, H, D), dtype=np.float32))
+    v = W.bf16_round(rng.standard_normal((Lk, H, D), dtype=np.float32))
+    S = wl.S
+    uv = np.stack([rng.uniform(0, wl.w, (S, Lq)), rng.uniform(0, wl.h, (S, Lq))], -1).astype(np.float32)
+    idx = rng.integers(-2, wl.h * wl.w, (S, Lq)).astype(np.int32)
+    o, lse = _run(q8, k8, v, wl.slot, uv, idx, wl.h, wl.w, wl.softmax_scale)
+    rows = sample_rows(Lq, 48)
+    Oo, Lo = OA.biased_attention(OA.fp8e4m3_values(q8), OA.fp8e4m3_values(k8), v, wl.slot, uv, idx, wl.h, wl.w,
+                                 wl.softmax_scale, wl.lam, wl.sigma, rows=rows)
+    err = np.abs(host(o)[rows] - Oo).max()
+    lerr = np.abs(host(lse)[:, rows] - Lo).max()
+    print(f"fp8 logits, history bank: max|dO|={err:.3e} max|dLSE|={lerr:.3e}")
+    assert err <= BF16_TOL and lerr <= LSE_BF16_TOL

@@ -155,3 +155,16 @@ def test_brute_force_agrees_on_tiny_workload():
                                      c1.lam, c1.sigma)
         np.testing.assert_allclose(O[r, 0], out, atol=1e-12)
         assert abs(lse[0, r] - l) < 1e-12
+
+
+def test_fp8e4m3_decoding_matches_torch_on_every_code():
+    """The oracle's e4m3 decoding (fp8-logit attention inputs) against torch's
+    float8_e4m3fn for all 256 codes, plus hand values."""
+    import torch
+    from oracle.attention import fp8e4m3_values
+    codes = np.arange(256, dtype=np.uint8)
+    got = fp8e4m3_values(codes)
+    want = torch.from_numpy(codes).view(torch.float8_e4m3fn).float().numpy().astype(np.float64)
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+    assert np.array_equal(got[~np.isnan(got)], want[~np.isnan(want)])
+    assert fp8e4m3_values(np.array([0x38, 0x7E, 0x01, 0xC4, 0x08]), ).tolist() == [1.0, 448.0, 2.0**-9, -3.0, 2.0**-6]

@@ -66,3 +66,13 @@ def test_reproj_batch_tiles_distinct_problems():
     assert arrs[0].shape == (40, 3, 60, 104) and arrs[3].shape == (40, 6, 60, 104)
     assert np.array_equal(arrs[0][3], arrs[0][11])
     assert not np.array_equal(arrs[0][3], arrs[0][4])
+
+
+def test_fp8e4m3_encoding_matches_torch():
+    import torch
+    from workloads.synth import fp8e4m3_bits
+    rng = np.random.default_rng(1)
+    x = np.concatenate([rng.standard_normal(50000).astype(np.float32) * s for s in (1.0, 0.01, 30.0)] +
+                       [np.array([0.0, -0.0, 448.0, -448.0, 2.0**-9, 2.0**-10, 3 * 2.0**-10, -1e-5], np.float32)])
+    want = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(fp8e4m3_bits(x), want)

@@ -35,6 +35,22 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
     return out
 
 
+def fp8e4m3_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 -> fp8 e4m3 codes (uint8), round to nearest even, saturating at
+    +-448 (inputs are finite)."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(x), 448.0)
+    _, e = np.frexp(a)  # a = f 2^e, 0.5 <= f < 1: spacing 2^(e - 4), at least 2^-9
+    q = np.maximum(e - 4, -9)
+    r = np.rint(np.ldexp(a, -q))  # ties to even
+    v = np.ldexp(r, q)
+    _, e2 = np.frexp(v)
+    exp_field = np.where(v >= 2.0**-6, e2 - 1 + 7, 0)
+    mant = np.where(v >= 2.0**-6, np.rint((np.ldexp(v, -(e2 - 1)) - 1.0) * 8), np.rint(v / 2.0**-9))
+    code = (exp_field.astype(np.int64) << 3) | mant.astype(np.int64)
+    return (code | np.where(np.signbit(x), 0x80, 0)).astype(np.uint8)
+
+
 def bf16_round(x: np.ndarray) -> np.ndarray:
     """fp32 values rounded to the nearest bf16, returned as fp32."""
     bits = bf16_bits(x).astype(np.uint32) << 16
