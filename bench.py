@@ -41,6 +41,7 @@ if ROOT not in sys.path:
 METRIC = "biased-attention TFLOP/s + MFMA util; reprojection tokens/s (Wan-1.3B shape)"
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+FP8_BF16_PEAK_TFLOPS = 2.0 / (1.0 / 5000.0 + 1.0 / 2500.0)  # half the flops at the fp8 peak, half at bf16
 BENCH_QUERY = 1  # query chunk n = 225: a full top-4 retrieval
 PACK_LAYERS = 30  # transformer blocks of the 1.3B backbone: one packing call covers all of them
 ROPE_T_PAIRS, ROPE_THETA = 22, 10000.0  # temporal band of the factorised 3-D RoPE at head dim 128
@@ -192,6 +193,30 @@ def main():
 
     # sanity: the step produced a full retrieval and finite outputs
     assert int(rcount.item()) == r.k and torch.isfinite(o.float()).all()
+
+    # fp8 logits: the same chunk with q and k in fp8 e4m3 (v, o bf16). Half the flops (Q K^T) run on the
+    # fp8 matrix cores, half (P V) on bf16 ones: the time-weighted peak is 2 / (1/5000 + 1/2500) TFLOP/s
+    q8, k8 = q.float().to(torch.float8_e4m3fn), k.float().to(torch.float8_e4m3fn)
+    o8 = torch.empty_like(o)
+    lse8 = torch.empty_like(lse)
+
+    def attn8():
+        rv.biased_chunk_attention(q8, k8, v, slot, cuv[0], cidx[0], h=wl.h, w=wl.w, softmax_scale=wl.softmax_scale,
+                                  lam=wl.lam, sigma=wl.sigma, out=(o8, lse8))
+    for _ in range(3):
+        attn8()
+    e8a, e8b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e8a.record(stream)
+    for _ in range(args.steps):
+        attn8()
+    e8b.record(stream)
+    torch.cuda.synchronize()
+    a8_ms = e8a.elapsed_time(e8b) / args.steps
+    a8_tflops = flops / (a8_ms * 1e-3) / 1e12
+    a8_dev = float((o8.float() - o.float()).abs().max().item())
+    log(f"attention with fp8 logits {a8_ms:.3f} ms = {a8_tflops:.1f} TFLOP/s; max |O_fp8 - O_bf16| = {a8_dev:.2e}")
+    del q8, k8, o8, lse8
 
     # reprojection throughput: one launch over REPROJ_BATCH independent C3-shaped problems
     log(f"batched reprojection: {REPROJ_BATCH} problems")
@@ -380,6 +405,12 @@ def main():
                 "achieved_GBs": round(rb_gbs, 1), "peak_GBs": HBM_PEAK_GBS,
                 "frac": round(rb_gbs / HBM_PEAK_GBS, 4), "bound": "hbm",
                 "traffic": counters.get("reproject"),
+            },
+            "attention_fp8_logits": {
+                "note": "the bench chunk with q, k in fp8 e4m3 (v, o bf16): Q K^T on the fp8 matrix cores",
+                "ms": round(a8_ms, 4), "achieved": round(a8_tflops, 2), "unit": "TFLOP/s",
+                "peak": FP8_BF16_PEAK_TFLOPS, "frac": round(a8_tflops / FP8_BF16_PEAK_TFLOPS, 4),
+                "max_abs_dev_from_bf16_output": a8_dev,
             },
             "reprojection_batched_pooled": {
                 "note": "the batched problems on token depth pooled once per stored frame (pool_token_depth), p = 1",
