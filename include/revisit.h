@@ -206,7 +206,8 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
  *               lambda == 0 turns the bias off (pointers may then be NULL)
  *   softmax_scale > 0 (normally 1/sqrt(D)), sigma > 0, lambda finite.
  *   q, k, v, o must be 16-byte aligned and corr_uv 8-byte aligned
- *   (REVISIT_ERR_SHAPE otherwise).
+ *   (REVISIT_ERR_SHAPE otherwise). With the bias on, the bf16 and fp8 paths
+ *   take token grids of at most 256 x 256 (REVISIT_ERR_SHAPE otherwise).
  *
  * Lq == 0 is valid (nothing to do).
  *
@@ -329,7 +330,7 @@ int pool_token_depth(const float* depth, int32_t n_frames, int32_t h, int32_t w,
  *      the retrieved frames carrying slots 0..F-1 when a chunk was retrieved.
  *
  * rc_stream_create -- allocates the stream on the current device.
- *   dtype REVISIT_BF16 (D = 128) or REVISIT_F32 (D = 64 or 128); 1 <= F <= 64;
+ *   dtype REVISIT_BF16 (D = 128, h, w <= 256) or REVISIT_F32 (D = 64 or 128); 1 <= F <= 64;
  *   capacity >= 5 (keeps chunk n-3 resident); method parameters as for the
  *   stage entry points. Allocation failure: REVISIT_ERR_MEMORY, nothing kept.
  *   Device memory: layers * capacity * F h w * H * D * 2 (K and V) elements

@@ -38,6 +38,7 @@ bool aligned(const void* ptr, uintptr_t bytes) { return ((uintptr_t)ptr % bytes)
 
 constexpr int64_t kMaxElems = (int64_t)1 << 40;
 constexpr int kMaxFrames = 1024;
+constexpr int kMaxGridSide = 256;  // token-grid rows / columns of the bf16 kernel's bias tables
 constexpr int kMaxKeyParts = 64;
 
 // key parts of the bf16 attention kernel; 0 = chosen per call
@@ -193,6 +194,10 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     if (!finite(gamma)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: lambda / (2 sigma^2 scale) overflows");
     if (Lq == 0) return REVISIT_OK;
     const bool bias = S > 0 && lambda != 0.0f;
+    // the bf16 / fp8 kernel keeps per-column and per-row bias operands of the token grid in LDS
+    if (bias && dtype != REVISIT_F32 && (h > kMaxGridSide || w > kMaxGridSide))
+        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: bf16 / fp8 with bias needs h, w <= %d (got %d x %d)",
+                    kMaxGridSide, h, w);
     if (!q || !k || !v || !o) return fail(REVISIT_ERR_NULL, "biased_chunk_attention: q, k, v and o are required");
     if (bias && (!kv_frame_slot || !corr_uv || !corr_idx))
         return fail(REVISIT_ERR_NULL, "biased_chunk_attention: slot table and correspondence map are required when S > 0");

@@ -118,6 +118,8 @@ int rc_stream_create(const rc_stream_config* cfg, rc_stream** out) {
         return revisit::fail_status(REVISIT_ERR_UNSUPPORTED, "rc_stream_create: head dim %d not supported for this dtype", c.D);
     if (c.F < 1 || c.F > 64 || c.h < 1 || c.w < 1 || c.p < 1 || c.H < 1 || c.layers < 1 || c.max_chunks < 1)
         return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_create: need 1 <= F <= 64 and h, w, p, H, layers, max_chunks >= 1");
+    if (c.dtype == REVISIT_BF16 && (c.h > 256 || c.w > 256))
+        return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_create: bf16 attention with bias needs h, w <= 256");
     if (c.capacity < 5 || c.capacity > (1 << 20))
         return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_create: capacity %d outside [5, 2^20]", c.capacity);
     const int64_t T = (int64_t)c.F * c.h * c.w;

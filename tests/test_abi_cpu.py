@@ -116,7 +116,7 @@ def _attention(L, **kw):
     (dict(dtype=7), 3), (dict(D=64), 3), (dict(dtype=2, D=96), 3), (dict(Lk=28081), 2), (dict(Lk=0), 2),
     (dict(H=0), 2), (dict(Lq=-1), 2), (dict(sigma=0.0), 4), (dict(scale=-1.0), 4), (dict(lam=float("inf")), 4),
     (dict(sigma=1e-30), 4), (dict(q=NULL), 1), (dict(o=NULL), 1), (dict(uv=NULL), 1), (dict(slot=NULL), 1),
-    (dict(Lk=1025 * 1560), 2),
+    (dict(Lk=1025 * 1560), 2), (dict(h=300, w=4, Lk=1200 * 8), 2), (dict(dtype=3, h=4, w=257, Lk=1028 * 8), 2),
 ])
 def test_attention_rejects(L, kw, status):
     assert _attention(L, **kw) == status
@@ -177,7 +177,7 @@ def _stream_cfg(**kw):
     (dict(dtype=5), 3), (dict(D=64), 3), (dict(dtype=2, D=96), 3), (dict(F=0), 2), (dict(F=65), 2), (dict(h=0), 2),
     (dict(layers=0), 2), (dict(capacity=4), 2), (dict(max_chunks=0), 2), (dict(E=0.0), 4),
     (dict(sigma=float("nan")), 4), (dict(eps=-1.0), 4), (dict(softmax_scale=0.0), 4), (dict(rope_t_pairs=65), 4),
-    (dict(rope_theta=-1.0), 4),
+    (dict(rope_theta=-1.0), 4), (dict(w=257), 2),
 ])
 def test_stream_create_rejects(L, kw, status):
     h = ctypes.c_void_p(0x1234)

@@ -469,3 +469,24 @@ def test_empty_query_chunk_is_noop():
     o, lse = rv.biased_chunk_attention(q, k, k, dev(np.full(2, -1, np.int32)), None, None, h=4, w=5,
                                        softmax_scale=0.1, lam=1.0, sigma=2.0)
     assert o.shape == (0, 2, 128) and lse.shape == (2, 0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_attention_beyond_staged_frames_and_widest_grid(dtype):
+    """Bias edges of the bf16 kernel: 20 retrieved frames (correspondences of
+    frames 16.. are loaded on demand, the first 16 come from LDS), and a token
+    grid 256 wide (the largest its per-column bias table holds)."""
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    tol, ltol = (F32_TOL, LSE_F32_TOL) if dtype == "f32" else (BF16_TOL, LSE_BF16_TOL)
+    for (Lq, nf, H, h, w, S) in ((150, 24, 2, 4, 5, 20), (130, 4, 1, 2, 256, 2)):
+        rng = np.random.default_rng(nf * 31 + w)
+        Lk = nf * h * w
+        q, k, v, slot, uv, idx = _synthetic(rng, Lq, Lk, H, 128, h, w, S, dtype)
+        slot = np.full(nf, -1, np.int32)
+        slot[nf - S:] = np.arange(S)  # the retrieved frames last, frames >= 16 included
+        o, lse = rv.biased_chunk_attention(dev(q, tdt), dev(k, tdt), dev(v, tdt), dev(slot), dev(uv), dev(idx), h=h,
+                                           w=w, softmax_scale=1.0 / math.sqrt(128), lam=1.0, sigma=2.0)
+        Oo, Lo = OA.biased_attention(q, k, v, slot, uv, idx, h, w, 1.0 / math.sqrt(128), 1.0, 2.0)
+        err, lerr = np.abs(host(o) - Oo).max(), np.abs(host(lse) - Lo).max()
+        print(f"{dtype} S={S} grid {h}x{w}: max|dO|={err:.3e} max|dLSE|={lerr:.3e}")
+        assert err <= tol and lerr <= ltol
