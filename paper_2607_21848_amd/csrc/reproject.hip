@@ -35,6 +35,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kMaxSrcLds = 64;  // source frames per problem
+constexpr int64_t kSmallLaunch = 512;  // token blocks below which a block takes one source
 
 // Mean of the p x p depth block of token (i, j): rows outer, columns inner.
 // P = 1 or 2: compile-time block; P = 0: runtime p.
@@ -142,15 +143,24 @@ __device__ __forceinline__ Corr correspond(const ReprojectArgs& a, const Lifted&
     return Corr{uv, (Zs <= tol * Ds) ? ky * a.w + kx : -4};
 }
 
-template <int P>
+// kPerSource = false: a thread handles one token and loops over the S
+// source frames (the lift is done once). kPerSource = true: a thread handles
+// one (token, source) pair, for launches too small to fill the GPU with one
+// thread per token; the arithmetic and its order are the same.
+template <int P, bool kPerSource>
 __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const int hw = a.h * a.w;
     const int blocks_per_frame = (hw + kBlock - 1) / kBlock;
-    // work item = (problem, target frame, token block), problem-major, each XCD a
-    // contiguous range so one problem's source depth stays in one L2
-    const unsigned n_items = (unsigned)(blocks_per_frame * a.B * a.Tq);
-    const int item = (int)__builtin_amdgcn_readfirstlane(xcd_item(blockIdx.x, n_items));
-    if (item >= (int)n_items) return;  // grid padding (uniform, before the barrier)
+    // work item = (problem, target frame, token block[, source]), problem-major,
+    // each XCD a contiguous range so one problem's source depth stays in one L2
+    const int per_item_src = kPerSource ? a.S : 1;
+    const unsigned n_items = (unsigned)(blocks_per_frame * a.B * a.Tq * per_item_src);
+    const int item_all = (int)__builtin_amdgcn_readfirstlane(xcd_item(blockIdx.x, n_items));
+    if (item_all >= (int)n_items) return;  // grid padding (uniform, before the barrier)
+    const int s_item = kPerSource ? item_all % a.S : 0;
+    const int item = kPerSource ? item_all / a.S : item_all;
+    const int s_begin = kPerSource ? s_item : 0;
+    const int s_end = kPerSource ? s_item + 1 : a.S;
     // (problem, target frame) of this block; uniform, kept in scalar registers
     const int bt = __builtin_amdgcn_readfirstlane(item / blocks_per_frame);  // b * Tq + t
     const int b = __builtin_amdgcn_readfirstlane(bt / a.Tq);
@@ -172,9 +182,9 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const Lifted L = lift<P>(pooled<P>(a.tgt_depth + (size_t)bt * frame_px, Wd, i, j, p), i, j, fxt, fyt, cxt, cyt, Mt);
     const double tol = 1.0 + a.eps;
 
-    // the problem's source frames, converted once per block
+    // the problem's source frames (this block's one with kPerSource), converted once per block
     __shared__ SrcFrames sf;
-    for (int s = threadIdx.x; s < a.S; s += kBlock) {
+    for (int s = s_begin + threadIdx.x; s < s_end; s += kBlock) {
         int f = b * a.S + s;
         if (a.src_sel) {
             f = a.src_sel[(size_t)b * a.S + s];
@@ -194,7 +204,7 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     __syncthreads();
     if (tok >= hw) return;
 
-    for (int s = 0; s < a.S; ++s) {
+    for (int s = s_begin; s < s_end; ++s) {
         const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
         const Corr c = correspond<P>(a, L, sf, s, Wd, frame_px, p, tol);
         st_uv(reinterpret_cast<float2*>(a.out_uv) + o, c.uv);
@@ -204,19 +214,29 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
 
 }  // namespace
 
+template <bool kPerSource>
+static void launch_p(const ReprojectArgs& a, dim3 grid, hipStream_t stream) {
+    const dim3 block(kBlock);
+    if (a.p == 2) {
+        hipLaunchKernelGGL((reproject_kernel<2, kPerSource>), grid, block, 0, stream, a);
+    } else if (a.p == 1) {
+        hipLaunchKernelGGL((reproject_kernel<1, kPerSource>), grid, block, 0, stream, a);
+    } else {
+        hipLaunchKernelGGL((reproject_kernel<0, kPerSource>), grid, block, 0, stream, a);
+    }
+}
+
 hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream) {
     const int hw = a.h * a.w;
     if (a.B == 0 || a.Tq == 0 || a.S == 0 || hw == 0) return hipSuccess;
     const int64_t blocks = (int64_t)((hw + kBlock - 1) / kBlock) * a.B * a.Tq;
-    if (blocks > INT32_MAX - kXcds) return hipErrorInvalidValue;
-    const dim3 grid(xcd_grid((unsigned)blocks)), block(kBlock);
-    if (a.p == 2) {
-        hipLaunchKernelGGL(reproject_kernel<2>, grid, block, 0, stream, a);
-    } else if (a.p == 1) {
-        hipLaunchKernelGGL(reproject_kernel<1>, grid, block, 0, stream, a);
-    } else {
-        hipLaunchKernelGGL(reproject_kernel<0>, grid, block, 0, stream, a);
-    }
+    // fewer token blocks than two per compute unit: one block per (token block, source)
+    const bool per_source = a.S > 1 && blocks < kSmallLaunch;
+    const int64_t grid_blocks = per_source ? blocks * a.S : blocks;
+    if (grid_blocks > INT32_MAX - kXcds) return hipErrorInvalidValue;
+    const dim3 grid(xcd_grid((unsigned)grid_blocks));
+    if (per_source) launch_p<true>(a, grid, stream);
+    else launch_p<false>(a, grid, stream);
     return hipGetLastError();
 }
 

@@ -211,6 +211,24 @@ def test_reprojection_batched_and_no_source():
     assert (gidx[0, 2] == -5).all() and (gidx[1, 1] == -5).all() and (gidx[1, 3] == -5).all()
 
 
+def test_reprojection_per_token_and_per_source_launches_agree():
+    """A launch of 32 problems runs one thread per token (looping over the
+    sources); a launch of one problem, too small to fill the GPU that way,
+    runs one thread per (token, source). Both give the same bits, and the
+    oracle's on sampled problems."""
+    B = 32
+    arrs = W.make_reproj_batch(B, distinct=4)
+    guv, gidx = rv.reproject_correspondence(*[dev(a) for a in arrs], p=2, eps=0.05)
+    guv, gidx = host(guv), host(gidx)
+    for b in range(B):
+        suv, sidx = rv.reproject_correspondence(*[dev(a[b:b + 1]) for a in arrs], p=2, eps=0.05)
+        assert np.array_equal(host(sidx)[0], gidx[b])
+        assert np.array_equal(host(suv)[0].view(np.uint32), guv[b].view(np.uint32))
+    for b in (0, 3, 31):
+        ouv, oidx = OR.reproject(*[a[b] for a in arrs], 2, 0.05)
+        _compare_reprojection(ouv, oidx, guv[b], gidx[b], 2, 30, 52, f"batch-32 problem {b}")
+
+
 def test_pooled_depth_and_reprojection_on_pooled_maps():
     """pool_token_depth bit-exact against the oracle's pooling rounded to fp32
     (NaN, inf, zero and negative pixels included); reprojection with p = 1 on
