@@ -66,8 +66,10 @@ def profiled_counters():
             sha = hashlib.sha256(f.read()).hexdigest()[:16]
         if c.get(f"{key}_sha") == sha:
             out[key] = c[f"{key}_traffic_bytes"]
-    if "attention" in out and "mfma_busy_fraction" in c:
-        out["mfma_busy_fraction"] = c["mfma_busy_fraction"]
+    if "attention" in out:
+        for key in ("mfma_busy_fraction", "valu_busy_fraction"):
+            if key in c:
+                out[key] = c[key]
     return out
 
 
@@ -264,7 +266,21 @@ def main():
     rp_gbs = tokens * pooled_bytes_per_token / (rp_ms * 1e-3) / 1e9
     log(f"batched reprojection on pooled maps {rp_ms:.3f} ms: {tokens / (rp_ms * 1e-3):.3e} tokens/s, "
         f"{rp_gbs:.0f} GB/s algorithmic")
-    del bt, buv, bidx, pt, ps, pargs_r
+    # single-call latency at the exact C3 shape (one problem: 3 query frames x 6 sources): median of 50
+    # per-call event pairs after 10 warm-up calls
+    one = [x[:1] for x in bt]
+    for _ in range(10):
+        rv.reproject_correspondence(*one, p=p, eps=0.05, out=(buv[:1], bidx[:1]))
+    evs1 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(50)]
+    torch.cuda.synchronize()
+    for ea, eb in evs1:
+        ea.record(stream)
+        rv.reproject_correspondence(*one, p=p, eps=0.05, out=(buv[:1], bidx[:1]))
+        eb.record(stream)
+    torch.cuda.synchronize()
+    r1_us = float(np.median([ea.elapsed_time(eb) for ea, eb in evs1])) * 1e3
+    log(f"reprojection single call at the C3 shape: {r1_us:.1f} us (median of 50)")
+    del bt, buv, bidx, pt, ps, pargs_r, one
 
     # retrieval bandwidth on a stress bank far larger than the configs' (2^23 poses = 512 MiB)
     from workloads.synth import ring_bank
@@ -389,6 +405,7 @@ def main():
             "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
             "traffic": counters.get("attention"),
             "mfma_busy_profiled": counters.get("mfma_busy_fraction"),
+            "valu_busy_profiled": counters.get("valu_busy_fraction"),
             "flops_per_launch": flops,
             "avg_launch_ms": round(attn_ms, 4),
         },
@@ -396,6 +413,7 @@ def main():
             "retrieval_us": round(retr_ms * 1e3, 2),
             "reprojection_us": round(repr_ms * 1e3, 2),
             "reprojection_tokens_per_s_single_chunk": round(wl.Lq / (repr_ms * 1e-3), 0),
+            "reprojection_c3_single_call_us": round(r1_us, 2),
             "attention_ms": round(attn_ms, 4),
             "attention_tflops": round(attn_tflops, 2),
             "reprojection_batched": {

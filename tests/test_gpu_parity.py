@@ -227,6 +227,24 @@ def test_reprojection_per_token_and_per_source_launches_agree():
     for b in (0, 3, 31):
         ouv, oidx = OR.reproject(*[a[b] for a in arrs], 2, 0.05)
         _compare_reprojection(ouv, oidx, guv[b], gidx[b], 2, 30, 52, f"batch-32 problem {b}")
+    # the same with source frames selected from a shared bank (empty and out-of-range slots included)
+    bank = [dev(a.reshape(-1, *a.shape[2:])) for a in arrs[3:]]
+    n_bank = B * arrs[3].shape[1]
+    rng = np.random.Generator(np.random.PCG64(77))
+    sel = rng.integers(-2, n_bank + 3, size=(B, 6)).astype(np.int32)
+    tgt = [dev(a) for a in arrs[:3]]
+    guv, gidx = rv.reproject_correspondence(*tgt, *bank, p=2, eps=0.05, src_sel=dev(sel))
+    guv, gidx = host(guv), host(gidx)
+    for b in range(B):
+        suv, sidx = rv.reproject_correspondence(*[t[b:b + 1] for t in tgt], *bank, p=2, eps=0.05,
+                                                src_sel=dev(sel[b:b + 1]))
+        assert np.array_equal(host(sidx)[0], gidx[b])
+        assert np.array_equal(host(suv)[0].view(np.uint32), guv[b].view(np.uint32))
+    bank_h = [a.reshape(-1, *a.shape[2:]) for a in arrs[3:]]
+    for b in (1, 30):
+        sel_b = np.where((sel[b] >= 0) & (sel[b] < n_bank), sel[b], -1)
+        ouv, oidx = OR.reproject(arrs[0][b], arrs[1][b], arrs[2][b], *bank_h, 2, 0.05, src_sel=sel_b)
+        _compare_reprojection(ouv, oidx, guv[b], gidx[b], 2, 30, 52, f"batch-32 bank problem {b}")
 
 
 def test_pooled_depth_and_reprojection_on_pooled_maps():
