@@ -73,6 +73,13 @@ def retrieve_chunks(bank_c2w: torch.Tensor, query_c2w: torch.Tensor, query_chunk
                if frames_per_chunk is not None else None)
     else:
         idx, score, count, sel = out
+        _need(idx, "out idx", torch.int32, (Q, k), dev)
+        _need(score, "out score", torch.float32, (Q, k), dev)
+        _need(count, "out count", torch.int32, (Q,), dev)
+        if (sel is None) != (frames_per_chunk is None):
+            raise ValueError("out frame_sel must be given exactly when frames_per_chunk is")
+        if sel is not None:
+            _need(sel, "out frame_sel", torch.int32, (Q, k * frames_per_chunk), dev)
     st = lib().retrieve_chunks(_ptr(bank_c2w), N, _ptr(query_c2w), _ptr(query_chunk), Q, E, w_v, tau_c, tau_v,
                                delta, first_candidate, k, _ptr(idx), _ptr(score), _ptr(count),
                                frames_per_chunk or 0, _ptr(sel), _stream(dev))
@@ -159,7 +166,9 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
     _need(q, "q", q.dtype, None, dev)
     _need(k, "k", q.dtype, (Lk, H, D), dev)
     _need(v, "v", vdt, (Lk, H, D), dev)
-    _need(kv_frame_slot, "kv_frame_slot", torch.int32, None, dev)
+    if Lk % (h * w):
+        raise ValueError(f"Lk={Lk} is not a whole number of {h}x{w} frames")
+    _need(kv_frame_slot, "kv_frame_slot", torch.int32, (Lk // (h * w),), dev)
     S = 0
     if corr_uv is not None:
         S = corr_uv.shape[0]
