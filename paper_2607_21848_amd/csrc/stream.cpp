@@ -126,6 +126,16 @@ int rc_stream_create(const rc_stream_config* cfg, rc_stream** out) {
     if (T * 5 > (1 << 30) || (int64_t)c.h * c.p > (1 << 20) || (int64_t)c.w * c.p > (1 << 20) ||
         (int64_t)c.max_chunks > (1 << 30))
         return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_create: chunk too large");
+    if (c.H > 65535 || c.layers > (1 << 16))
+        return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_create: need H <= 65535 and layers <= 65536");
+    // the ring's rows of one layer are addressed with 32-bit row indices
+    if ((int64_t)c.capacity * T > INT32_MAX)
+        return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_create: capacity x tokens per chunk above 2^31 - 1");
+    // keys and values of the ring and the cache: at most 2^50 bytes each (no size_t overflow below)
+    const double kv_ring_bytes = (double)c.layers * c.capacity * (double)T * c.H * c.D * 4.0;
+    const double kv_cache_bytes = (double)c.layers * 5.0 * (double)T * c.H * c.D * 4.0;
+    if (kv_ring_bytes > 1125899906842624.0 || kv_cache_bytes > 1125899906842624.0)
+        return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_create: ring or cache above 2^50 bytes");
     if (!(is_finite(c.E) && c.E > 0.0f) || !is_finite(c.w_v) || !is_finite(c.tau_c) || !is_finite(c.tau_v) ||
         !(is_finite(c.eps) && c.eps >= 0.0f) || !is_finite(c.lambda) || !(is_finite(c.sigma) && c.sigma > 0.0f) ||
         !(is_finite(c.softmax_scale) && c.softmax_scale > 0.0f))

@@ -177,7 +177,8 @@ def _stream_cfg(**kw):
     (dict(dtype=5), 3), (dict(D=64), 3), (dict(dtype=2, D=96), 3), (dict(F=0), 2), (dict(F=65), 2), (dict(h=0), 2),
     (dict(layers=0), 2), (dict(capacity=4), 2), (dict(max_chunks=0), 2), (dict(E=0.0), 4),
     (dict(sigma=float("nan")), 4), (dict(eps=-1.0), 4), (dict(softmax_scale=0.0), 4), (dict(rope_t_pairs=65), 4),
-    (dict(rope_theta=-1.0), 4), (dict(w=257), 2),
+    (dict(rope_theta=-1.0), 4), (dict(w=257), 2), (dict(H=65536), 2), (dict(layers=70000), 2),
+    (dict(capacity=1 << 20, F=64, h=256, w=256), 2), (dict(layers=65536, H=65535), 2),
 ])
 def test_stream_create_rejects(L, kw, status):
     h = ctypes.c_void_p(0x1234)
