@@ -9,8 +9,11 @@ Bars (written here, not derived from the kernels):
   expressions);
 * attention: max |O - O_oracle| <= 1e-4 for fp32 inputs and <= 2e-2 for
   bf16 inputs (fp32 accumulation), |LSE - LSE_oracle| <= 1e-4 (fp32) and
-  <= 2e-3 (bf16: the logits see exact bf16 inputs, only the bias is
-  evaluated through split bf16 factors). The bf16 gate alone cannot see a
+  <= 4e-3 (bf16). The bf16 LSE bar follows from the arithmetic: the row sum
+  adds the probabilities as rounded to bf16 for P V, each off by at most the
+  bf16 unit roundoff 2^-8, so LSE can be off by up to ln(1 + 2^-8) = 3.9e-3
+  (the logits themselves see exact bf16 inputs and fp32 bias factors, ~1e-5).
+  The bf16 gate alone cannot see a
   bias-geometry error (dropping the bias moves O by ~4e-2), so every
   bias-carrying workload is also run with fp32 inputs at the 1e-4 bar and
   the LSE bar applies to bf16 too.
@@ -32,7 +35,7 @@ from tests.gpu_helpers import dev, dev_bf16, host, qkv_dev, sample_rows, same_bi
 pytestmark = pytest.mark.gpu
 
 F32_TOL, BF16_TOL = 1e-4, 2e-2
-LSE_F32_TOL, LSE_BF16_TOL = 1e-4, 2e-3
+LSE_F32_TOL, LSE_BF16_TOL = 1e-4, 4e-3
 
 
 @pytest.fixture(scope="module", autouse=True)

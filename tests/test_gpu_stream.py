@@ -9,7 +9,7 @@ against the oracle, stage by stage, from the driver's own buffers:
 * packed cache: values bit for bit, keys bit-exact in bf16 and within 1 ulp
   in fp32 (as for pack_retrieved_kv);
 * attention output and LSE: the bars of biased_chunk_attention (1e-4 fp32;
-  2e-2 / 2e-3 bf16).
+  2e-2 / 4e-3 bf16).
 Capacities 10 (loop closures retrieved on the second lap) and 6 (the ring has
 evicted the revisited chunks: the retrieved slot extends the recent window).
 """
@@ -64,7 +64,7 @@ def test_stream_against_oracle(dtype, capacity):
                           rope_theta=st.rope_theta)
     T = st.F * st.h * st.w
     esize = 2 if bf16 else 4
-    o_tol, l_tol = (2e-2, 2e-3) if bf16 else (1e-4, 1e-4)
+    o_tol, l_tol = (2e-2, 4e-3) if bf16 else (1e-4, 1e-4)
     retrieved = 0
     try:
         for n, ch in enumerate(st.chunks):
