@@ -63,7 +63,7 @@ enum {
     REVISIT_ERR_UNSUPPORTED = 3, /* dtype / head dimension not built */
     REVISIT_ERR_PARAM = 4,       /* a method parameter is out of its domain */
     REVISIT_ERR_LAUNCH = 5,      /* the HIP runtime refused the launch */
-    REVISIT_ERR_MEMORY = 6       /* a stream object could not get its memory */
+    REVISIT_ERR_MEMORY = 6       /* device or host memory could not be allocated */
 };
 
 /* Element types of biased_chunk_attention (and of the other calls where they
@@ -221,7 +221,8 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
  * allocated with hipMalloc on the first call that needs it and grown by later
  * calls that need more (after synchronising that stream). Calls queued on one
  * stream share its block in order; calls on different streams never share
- * one. A failed allocation returns REVISIT_ERR_LAUNCH with nothing enqueued.
+ * one. A failed allocation returns REVISIT_ERR_MEMORY (another HIP error
+ * while getting the block, REVISIT_ERR_LAUNCH) with nothing enqueued.
  */
 int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
                            float* lse, int32_t dtype,

@@ -116,7 +116,9 @@ int retrieve_chunks(const float* bank_c2w, int32_t n_bank, const float* query_c2
             return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: n_bank * n_query too large");
         void* ws = nullptr;
         const hipError_t e = revisit::stream_workspace(stream, revisit::retrieve_workspace_bytes(n_bank, n_query, k), &ws);
-        if (e != hipSuccess) return fail(REVISIT_ERR_LAUNCH, "retrieve_chunks: workspace: %s", hipGetErrorString(e));
+        if (e != hipSuccess)
+            return fail(e == hipErrorOutOfMemory ? REVISIT_ERR_MEMORY : REVISIT_ERR_LAUNCH, "retrieve_chunks: workspace: %s",
+                        hipGetErrorString(e));
         a.seg_s = static_cast<double*>(ws);
         a.seg_j = reinterpret_cast<int32_t*>(a.seg_s + (size_t)a.n_seg * n_query * k);
     }
@@ -237,7 +239,9 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     parts = parts < (Lk + 31) / 32 ? parts : (Lk + 31) / 32;  // at least one key tile per part
     void* ws = nullptr;
     const hipError_t e = revisit::stream_workspace(stream, revisit::attention_bf16_workspace_bytes(a, parts), &ws);
-    if (e != hipSuccess) return fail(REVISIT_ERR_LAUNCH, "biased_chunk_attention: workspace: %s", hipGetErrorString(e));
+    if (e != hipSuccess)
+        return fail(e == hipErrorOutOfMemory ? REVISIT_ERR_MEMORY : REVISIT_ERR_LAUNCH,
+                    "biased_chunk_attention: workspace: %s", hipGetErrorString(e));
     return launched(revisit::launch_attention_bf16(a, parts, static_cast<float*>(ws), stream), "biased_chunk_attention");
 }
 

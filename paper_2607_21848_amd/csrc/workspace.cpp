@@ -6,6 +6,7 @@
 #include <stddef.h>
 
 #include <mutex>
+#include <new>
 #include <vector>
 
 #include <hip/hip_runtime.h>
@@ -56,7 +57,13 @@ hipError_t stream_workspace(hipStream_t stream, size_t bytes, void** out) {
     void* p = nullptr;
     e = hipMalloc(&p, bytes);
     if (e != hipSuccess) return e;
-    g_blocks.push_back(Block{dev, stream, p, bytes});
+    // no C++ exception may leave the library's C entry points
+    try {
+        g_blocks.push_back(Block{dev, stream, p, bytes});
+    } catch (const std::bad_alloc&) {
+        (void)hipFree(p);
+        return hipErrorOutOfMemory;
+    }
     *out = p;
     return hipSuccess;
 }
@@ -66,7 +73,13 @@ hipError_t device_compute_units(int* cus) {
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     std::lock_guard<std::mutex> lock(g_mutex);
-    if ((int)g_cus.size() <= dev) g_cus.resize(dev + 1, -1);
+    if ((int)g_cus.size() <= dev) {
+        try {
+            g_cus.resize(dev + 1, -1);
+        } catch (const std::bad_alloc&) {
+            return hipErrorOutOfMemory;
+        }
+    }
     if (g_cus[dev] < 0) {
         int n = 0;
         e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
