@@ -10,8 +10,9 @@ against the oracle, stage by stage, from the driver's own buffers:
   in fp32 (as for pack_retrieved_kv);
 * attention output and LSE: the bars of biased_chunk_attention (1e-4 fp32;
   2e-2 / 4e-3 bf16).
-Capacities 10 (loop closures retrieved on the second lap) and 6 (the ring has
-evicted the revisited chunks: the retrieved slot extends the recent window).
+Capacities 10 (loop closures retrieved on the second lap), 6 (the ring has
+evicted the revisited chunks: the retrieved slot extends the recent window)
+and 5, the smallest ring that still holds the extension chunk n - 3.
 """
 
 from __future__ import annotations
@@ -52,7 +53,7 @@ def _ordered(a: np.ndarray) -> np.ndarray:
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("capacity", [10, 6])
+@pytest.mark.parametrize("capacity", [10, 6, 5])
 def test_stream_against_oracle(dtype, capacity):
     st = make_stream(n_chunks=14, dtype=dtype)
     bf16 = dtype == "bf16"
