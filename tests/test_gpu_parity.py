@@ -250,6 +250,26 @@ def test_reprojection_per_token_and_per_source_launches_agree():
         _compare_reprojection(ouv, oidx, guv[b], gidx[b], 2, 30, 52, f"batch-32 bank problem {b}")
 
 
+@pytest.mark.parametrize("B", [1, 32])
+def test_reprojection_fixed_centre_sources(B):
+    """Cameras that turn in place: every source of a problem shares the
+    centre of its target frame 0 (c_t - c_s is exactly zero, where Eq.
+    reprojection reduces to a homography, Sec. 4.3), and in every other
+    problem frame 1 shares it too; one problem (a thread per (token, source))
+    and 32 (a thread per token), bit-exact against the oracle."""
+    arrs = [a.copy() for a in W.make_reproj_batch(B, distinct=4)]
+    tgt_d, tgt_c, tgt_k, src_d, src_c, src_k = arrs
+    S = src_c.shape[1]
+    src_c[:, :, :3, 3] = tgt_c[:, 0:1, :3, 3]
+    tgt_c[:, 1, :3, 3] = np.where(np.arange(B)[:, None] % 2 == 0, tgt_c[:, 0, :3, 3], tgt_c[:, 1, :3, 3])
+    guv, gidx = rv.reproject_correspondence(*[dev(a) for a in arrs], p=2, eps=0.05)
+    guv, gidx = host(guv), host(gidx)
+    for b in sorted({0, B // 2, B - 1}):
+        ouv, oidx = OR.reproject(*[a[b] for a in arrs], 2, 0.05)
+        _compare_reprojection(ouv, oidx, guv[b], gidx[b], 2, 30, 52, f"fixed centre, problem {b}")
+        assert (oidx >= 0).mean() > 0.3
+
+
 def test_pooled_depth_and_reprojection_on_pooled_maps():
     """pool_token_depth bit-exact against the oracle's pooling rounded to fp32
     (NaN, inf, zero and negative pixels included); reprojection with p = 1 on

@@ -9,7 +9,8 @@ lambda of either sign and zero, sigma, softmax scale, and forced key-part
 counts for the bf16 kernel. Correspondence: batches sized so that both
 launch shapes (a thread per token, a thread per (token, source)) occur,
 p = 1, 2, 3, depth maps with NaN, zero and negative pixels, with and
-without a frame-bank selection."""
+without a frame-bank selection, and sources that share a target frame's
+camera centre (a camera turning in place) mixed with ones that do not."""
 
 from __future__ import annotations
 
@@ -116,17 +117,19 @@ def _poses(rng, n, base):
     return out
 
 
-# (B, Tq, S, h, w, p, bank): large cases run a thread per token, small ones a thread per (token, source)
+# (B, Tq, S, h, w, p, bank, shared centres): large cases run a thread per token, small ones a thread
+# per (token, source)
 SWEEP_REPROJ = [
-    (40, 3, 6, 30, 40, 2, False), (48, 3, 8, 33, 27, 1, True), (1, 1, 1, 1, 1, 1, False), (3, 2, 5, 7, 11, 3, True),
-    (1, 3, 12, 30, 52, 2, True), (2, 1, 64, 5, 6, 2, False), (64, 3, 4, 25, 30, 3, False), (5, 1, 3, 40, 1, 2, True),
-    (7, 3, 2, 1, 40, 1, False), (90, 3, 6, 17, 29, 2, True),
+    (40, 3, 6, 30, 40, 2, False, False), (48, 3, 8, 33, 27, 1, True, False), (1, 1, 1, 1, 1, 1, False, False),
+    (3, 2, 5, 7, 11, 3, True, False), (1, 3, 12, 30, 52, 2, True, True), (2, 1, 64, 5, 6, 2, False, True),
+    (64, 3, 4, 25, 30, 3, False, True), (5, 1, 3, 40, 1, 2, True, True), (7, 3, 2, 1, 40, 1, False, False),
+    (90, 3, 6, 17, 29, 2, True, True),
 ]
 
 
 @pytest.mark.parametrize("case", range(len(SWEEP_REPROJ)))
 def test_reprojection_random_sweep(case):
-    B, Tq, S, h, w, p, bank = SWEEP_REPROJ[case]
+    B, Tq, S, h, w, p, bank, shared = SWEEP_REPROJ[case]
     rng = np.random.default_rng(9300 + case)
     eps = float(rng.choice([0.0, 0.05, 0.2]))
     base = pose_from(axis_angle(random_unit(rng), rng.uniform(0, math.pi)), rng.normal(size=3))
@@ -135,11 +138,20 @@ def test_reprojection_random_sweep(case):
     n_src = B * S if not bank else int(rng.integers(max(1, S // 2), 3 * S + 2))
     sd, sk = _scene(rng, n_src, h, w, p)
     sc = _poses(rng, n_src, base)
+    sel = rng.integers(-2, n_src + 2, size=(B, S)).astype(np.int32) if bank else None
+    if shared:  # sources at the centre of one of their problem's target frames (turning in place)
+        if bank:
+            for b in range(B):
+                if 0 <= sel[b, 0] < n_src:
+                    sc[sel[b, 0], :3, 3] = tc[b * Tq + int(rng.integers(0, Tq)), :3, 3]
+        else:
+            for f in range(0, n_src, 2):
+                sc[f, :3, 3] = tc[(f // S) * Tq + int(rng.integers(0, Tq)), :3, 3]
     Hd, Wd = h * p, w * p
     tgt = (td.reshape(B, Tq, Hd, Wd), tc.reshape(B, Tq, 4, 4), tk.reshape(B, Tq, 4))
-    print(f"case {case}: B={B} Tq={Tq} S={S} grid {h}x{w} p={p} bank={bank} eps={eps}", flush=True)
+    print(f"case {case}: B={B} Tq={Tq} S={S} grid {h}x{w} p={p} bank={bank} shared centres={shared} eps={eps}",
+          flush=True)
     if bank:
-        sel = rng.integers(-2, n_src + 2, size=(B, S)).astype(np.int32)
         guv, gidx = rv.reproject_correspondence(*[dev(a) for a in tgt], dev(sd), dev(sc), dev(sk), p=p, eps=eps,
                                                 src_sel=dev(sel))
     else:
