@@ -633,6 +633,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // the operand of the frame the last biased tile lay in
     int qcur_f = -1;
     bf16x8 qcur = as_bf16x8(u32x4{0, 0, 0, 0});
+    // slot of the frame the last fast-path tile lay in (uniform): looked up again only when the frame changes
+    int scur_f = -1, scur = -1;
     // frame and in-frame offset of the next QK tile's first key (uniform)
     int blk_f = tile0 / g.hw, blk_t = tile0 - blk_f * g.hw;
     // this lane's key operand for in-frame key position t (< hw)
@@ -650,7 +652,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         floatx16 init = floatx16{0};
         const int span = min(31, Lk - 1 - k0);
         if (span == 31 && blk_t + 31 < g.hw) {
-            const int s = __builtin_amdgcn_readfirstlane(lds_slot[blk_f]);
+            if (scur_f != blk_f) {
+                scur = __builtin_amdgcn_readfirstlane(lds_slot[blk_f]);
+                scur_f = blk_f;
+            }
+            const int s = scur;
             if (s >= 0) {
                 if (qcur_f != blk_f) {
                     qcur = query_operand(s);
