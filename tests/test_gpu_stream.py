@@ -128,3 +128,35 @@ def test_stream_runs_out_of_bank():
         assert e.value.status == 2
     finally:
         drv.close()
+
+
+def test_stream_without_lse_and_two_streams_side_by_side():
+    """The LSE output is optional: a driver stepped without it gives the same
+    O, bit for bit, as one stepped with it. The two drivers run side by side
+    on the same device, each on its own HIP stream, which also checks that
+    their ring, cache and workspaces stay apart."""
+    st = make_stream(n_chunks=9, dtype="bf16")
+    kw = dict(F=st.F, h=st.h, w=st.w, p=st.p, H=st.H, D=st.D, layers=st.L, dtype=torch.bfloat16, capacity=10,
+              max_chunks=16, E=st.E, w_v=st.w_v, tau_c=st.tau_c, tau_v=st.tau_v, delta=st.delta, eps=st.eps,
+              lam=st.lam, sigma=st.sigma, softmax_scale=st.softmax_scale, rope_t_pairs=st.rope_t_pairs,
+              rope_theta=st.rope_theta)
+    a, b = rv.StreamDriver(**kw), rv.StreamDriver(**kw)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    T = st.F * st.h * st.w
+    try:
+        for ch in st.chunks:
+            ins = (_dev(ch.depth), _dev(ch.c2w), _dev(ch.K), _dev(ch.q, True), _dev(ch.k, True), _dev(ch.v, True))
+            oa = torch.empty((st.L, T, st.H, st.D), dtype=torch.bfloat16, device="cuda:0")
+            la = torch.empty((st.L, st.H, T), dtype=torch.float32, device="cuda:0")
+            ob = torch.empty_like(oa)
+            torch.cuda.synchronize()
+            with torch.cuda.stream(sa):
+                a.step(*ins, out=(oa, la))
+            with torch.cuda.stream(sb):
+                b.step(*ins, out=(ob, None))
+            torch.cuda.synchronize()
+            assert torch.equal(oa, ob)
+            assert torch.isfinite(la).all()
+    finally:
+        a.close()
+        b.close()
