@@ -2,7 +2,7 @@
 // (Sec. 4.3, Eq. reprojection and Eq. visibility; rejection causes of
 // design choice (iii)).
 //
-// Launch: one thread per query token; a 256-thread block covers 256 tokens
+// Launch: one thread per query token; a 128-thread block covers 128 tokens
 // of one (problem b, target frame t) pair. The pose and
 // intrinsics of (b, t) and of each source frame are wave-uniform, so they
 // arrive through scalar loads; the thread pools its token's p x p depth
@@ -33,7 +33,7 @@
 namespace revisit {
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = 128;  // measured 1-2% faster than 256 (and than 64, 512, 1024)
 constexpr int kMaxSrcLds = 64;  // source frames per problem
 constexpr int64_t kSmallLaunch = 512;  // token blocks below which a block takes one source
 
