@@ -27,10 +27,11 @@
  * - Every array argument is a DEVICE pointer owned by the caller and must
  *   stay valid until the work queued on `stream` has completed. Outputs must
  *   not alias inputs. State kept by the library: a per-thread last-error
- *   string, the setting of rc_set_attention_key_parts(), the bf16
- *   attention workspace described at biased_chunk_attention, and the
- *   device memory of stream objects (rc_stream_create), which the caller
- *   owns through the handle.
+ *   string, the setting of rc_set_attention_key_parts(), the per-stream
+ *   workspace described at biased_chunk_attention (used by the bf16 key
+ *   split and by the segmented retrieval of large banks), and the device
+ *   memory of stream objects (rc_stream_create), which the caller owns
+ *   through the handle.
  * - Calls are asynchronous on `stream` (NULL = the default stream).
  * - Arguments are validated on the host before anything is queued: on a
  *   non-zero status nothing has been enqueued and rc_last_error() says why.
