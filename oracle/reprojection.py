@@ -33,6 +33,10 @@ not these details):
 
 The output u^ is rounded to fp32 for tokens with reason >= 0, -3 or -4 and
 is NaN for -1, -2 and -5.
+
+``rotation_pair`` / ``reproject_rotation`` state the fixed-centre case of
+Eq. reprojection (the rotation / zoom homography of Sec. 4.3) as its own
+depth-free path; see their docstrings for the reading taken.
 """
 
 from __future__ import annotations
@@ -40,6 +44,7 @@ from __future__ import annotations
 import numpy as np
 
 UNDEFINED, BEHIND, OFF_GRID, OCCLUDED, NO_SOURCE = -1, -2, -3, -4, -5
+CENTRE_MOVED = -6  # rotation-only path: the source's centre is not the target's
 
 
 def pooled_depth(depth, p):
@@ -134,6 +139,87 @@ def reproject(tgt_depth, tgt_c2w, tgt_K, src_depth, src_c2w, src_K, p, eps, src_
             continue
         for t in range(Tq):
             u, i = reproject_pair(tgt_depth[t], tgt_c2w[t], tgt_K[t], src_depth[f], src_c2w[f], src_K[f], p, eps)
+            uv[s, t * h * w:(t + 1) * h * w] = u
+            idx[s, t * h * w:(t + 1) * h * w] = i
+    return uv, idx
+
+
+def rotation_pair(tgt_c2w, tgt_K, src_c2w, src_K, h, w, p):
+    """Correspondence of every token of ONE target frame into ONE source frame
+    that shares its camera centre: the rotation / zoom homography of Sec. 4.3.
+
+    With c_s = c_t the depth z_p scales X_s and cancels under pi, so Eq.
+    reprojection reduces to u^ = pi(K_s R_s^T R_t K_t^{-1} u~). This path reads
+    no depth: the visibility test of Eq. visibility is not applied (with one
+    centre there is no parallax, hence no disocclusion), so the codes are the
+    key index, -2 (behind the source camera), -3 (off the grid) or
+    CENTRE_MOVED (-6) for every token when the two fp32 centres are not equal.
+
+    The matrix is formed once per frame pair, in this order:
+        A = R_s^T R_t          A[r][c] = (Rs[0][r] Rt[0][c] + Rs[1][r] Rt[1][c]) + Rs[2][r] Rt[2][c]
+        M = K_s A              rows (fx_s A0 + cx_s A2, fy_s A1 + cy_s A2, A2)
+        H = M K_t^{-1}         H[r][0] = M[r][0] / fx_t, H[r][1] = M[r][1] / fy_t,
+                               H[r][2] = (M[r][2] - H[r][0] cx_t) - H[r][1] cy_t
+    then per token v_r = (H[r][0] u_x + H[r][1] u_y) + H[r][2] and
+    u^ = (v_0 / v_2, v_1 / v_2), behind iff v_2 <= 0 (v_2 has the sign of
+    [X_s]_z for any positive depth). Intrinsics on the token grid as for
+    ``reproject_pair``. Returns (uv [h*w, 2] float32, idx [h*w] int32)."""
+    Mt32 = np.asarray(tgt_c2w, dtype=np.float32)
+    Ms32 = np.asarray(src_c2w, dtype=np.float32)
+    n = h * w
+    if not bool(np.all(Mt32[:3, 3] == Ms32[:3, 3])):
+        return np.full((n, 2), np.nan, np.float32), np.full(n, CENTRE_MOVED, np.int32)
+    fxt, fyt, cxt, cyt = (float(x) for x in token_intrinsics(tgt_K, p))
+    fxs, fys, cxs, cys = (float(x) for x in token_intrinsics(src_K, p))
+    Rt = Mt32[:3, :3].astype(np.float64)
+    Rs = Ms32[:3, :3].astype(np.float64)
+    A = [[(Rs[0, r] * Rt[0, c] + Rs[1, r] * Rt[1, c]) + Rs[2, r] * Rt[2, c] for c in range(3)] for r in range(3)]
+    M = [[fxs * A[0][c] + cxs * A[2][c] for c in range(3)],
+         [fys * A[1][c] + cys * A[2][c] for c in range(3)],
+         [A[2][c] for c in range(3)]]
+    H = []
+    for r in range(3):
+        h0 = M[r][0] / fxt
+        h1 = M[r][1] / fyt
+        H.append((h0, h1, (M[r][2] - h0 * cxt) - h1 * cyt))
+
+    ii, jj = np.meshgrid(np.arange(h), np.arange(w), indexing="ij")
+    ux = jj.astype(np.float64) + 0.5
+    uy = ii.astype(np.float64) + 0.5
+    v0, v1, v2 = [(H[r][0] * ux + H[r][1] * uy) + H[r][2] for r in range(3)]
+    with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
+        uhx = v0 / v2
+        uhy = v1 / v2
+    front = v2 > 0
+    with np.errstate(invalid="ignore"):
+        on_grid = front & (uhx >= 0) & (uhx < w) & (uhy >= 0) & (uhy < h)
+    kx = np.where(on_grid, np.floor(np.where(on_grid, uhx, 0.0)), 0).astype(np.int64)
+    ky = np.where(on_grid, np.floor(np.where(on_grid, uhy, 0.0)), 0).astype(np.int64)
+    idx = np.where(on_grid, ky * w + kx, OFF_GRID)
+    idx = np.where(front, idx, BEHIND)
+    uv = np.stack([uhx, uhy], axis=-1)
+    uv[~front] = np.nan
+    return uv.reshape(n, 2).astype(np.float32), idx.reshape(n).astype(np.int32)
+
+
+def reproject_rotation(tgt_c2w, tgt_K, src_c2w, src_K, h, w, p, src_sel=None):
+    """``rotation_pair`` for all target frames against all source frames.
+
+    tgt_*: [Tq, ...]; src_*: [S, ...] (or a frame bank indexed by ``src_sel``
+    [S], an entry outside the bank = no source, NO_SOURCE). Returns uv
+    [S, Tq*h*w, 2] float32 and idx [S, Tq*h*w] int32."""
+    tgt_c2w = np.asarray(tgt_c2w)
+    Tq = tgt_c2w.shape[0]
+    n_bank = np.asarray(src_c2w).shape[0]
+    S = len(src_sel) if src_sel is not None else n_bank
+    uv = np.full((S, Tq * h * w, 2), np.nan, np.float32)
+    idx = np.full((S, Tq * h * w), NO_SOURCE, np.int32)
+    for s in range(S):
+        f = s if src_sel is None else int(src_sel[s])
+        if f < 0 or f >= n_bank:
+            continue
+        for t in range(Tq):
+            u, i = rotation_pair(tgt_c2w[t], tgt_K[t], src_c2w[f], src_K[f], h, w, p)
             uv[s, t * h * w:(t + 1) * h * w] = u
             idx[s, t * h * w:(t + 1) * h * w] = i
     return uv, idx
