@@ -61,7 +61,8 @@ def profiled_counters():
         c = json.load(f)
     src = os.path.join(ROOT, "paper_2607_21848_amd", "csrc")
     out = {}
-    for key, fname in (("attention", "attention.hip"), ("reproject", "reproject.hip"), ("kvpack", "kvpack.hip")):
+    for key, fname in (("attention", "attention.hip"), ("reproject", "reproject.hip"), ("rotation", "reproject.hip"),
+                       ("kvpack", "kvpack.hip")):
         with open(os.path.join(src, fname), "rb") as f:
             sha = hashlib.sha256(f.read()).hexdigest()[:16]
         if c.get(f"{key}_sha") == sha:
@@ -266,6 +267,22 @@ def main():
     rp_gbs = tokens * pooled_bytes_per_token / (rp_ms * 1e-3) / 1e9
     log(f"batched reprojection on pooled maps {rp_ms:.3f} ms: {tokens / (rp_ms * 1e-3):.3e} tokens/s, "
         f"{rp_gbs:.0f} GB/s algorithmic")
+    # rotation-only path: REPROJ_BATCH shared-centre problems (panorama-clip shape), no depth read; the
+    # algorithmic bytes are the S (u^ pair + code) written per token
+    rarrs = [t(a) for a in W.make_rotation_batch(REPROJ_BATCH)]
+    for _ in range(3):
+        rv.reproject_rotation(*rarrs, h=Hd // p, w=Wd // p, p=p, out=(buv, bidx))
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        rv.reproject_rotation(*rarrs, h=Hd // p, w=Wd // p, p=p, out=(buv, bidx))
+    e1.record(stream)
+    torch.cuda.synchronize()
+    rr_ms = e0.elapsed_time(e1) / reps
+    rot_bytes_per_token = S * 12
+    rr_gbs = tokens * rot_bytes_per_token / (rr_ms * 1e-3) / 1e9
+    log(f"batched rotation-only correspondence {rr_ms:.3f} ms: {tokens / (rr_ms * 1e-3):.3e} tokens/s, "
+        f"{rr_gbs:.0f} GB/s algorithmic")
     # single-call latency at the exact C3 shape (one problem: 3 query frames x 6 sources): median of 50
     # per-call event pairs after 10 warm-up calls
     one = [x[:1] for x in bt]
@@ -280,7 +297,7 @@ def main():
     torch.cuda.synchronize()
     r1_us = float(np.median([ea.elapsed_time(eb) for ea, eb in evs1])) * 1e3
     log(f"reprojection single call at the C3 shape: {r1_us:.1f} us (median of 50)")
-    del bt, buv, bidx, pt, ps, pargs_r, one
+    del bt, buv, bidx, pt, ps, pargs_r, one, rarrs
 
     # retrieval bandwidth on a stress bank far larger than the configs' (2^23 poses = 512 MiB)
     from workloads.synth import ring_bank
@@ -435,6 +452,14 @@ def main():
                 "ms": round(rp_ms, 4), "tokens_per_s": round(tokens / (rp_ms * 1e-3), 0),
                 "bytes_per_token": pooled_bytes_per_token, "achieved_GBs": round(rp_gbs, 1),
                 "peak_GBs": HBM_PEAK_GBS, "frac": round(rp_gbs / HBM_PEAK_GBS, 4), "bound": "hbm",
+            },
+            "reprojection_rotation_batched": {
+                "note": "rotation-only correspondence (shared camera centre, homography, no depth) on the same "
+                        "number of panorama-clip problems",
+                "ms": round(rr_ms, 4), "tokens_per_s": round(tokens / (rr_ms * 1e-3), 0),
+                "bytes_per_token": rot_bytes_per_token, "achieved_GBs": round(rr_gbs, 1),
+                "peak_GBs": HBM_PEAK_GBS, "frac": round(rr_gbs / HBM_PEAK_GBS, 4), "bound": "hbm",
+                "traffic": counters.get("rotation"),
             },
             "kv_pack": {
                 "layers": pack_layers, "chunks": r.k, "tokens_per_chunk": T_pack, "store_chunks": n_bank,

@@ -12,6 +12,9 @@
  *   reproject_correspondence  -- per-token depth/pose reprojection into the
  *                                retrieved frames with the occlusion test
  *                                (Sec. 4.3, Eq. reprojection, Eq. visibility)
+ *   reproject_rotation        -- the fixed-centre case of the same: the
+ *                                rotation / zoom homography, no depth
+ *                                (Sec. 4.3)
  *   biased_chunk_attention    -- chunk attention with the Gaussian
  *                                correspondence bias fused in
  *                                (Sec. 4.3, Eq. bias)
@@ -74,14 +77,17 @@ enum {
 enum { REVISIT_BF16 = 1, REVISIT_F32 = 2, REVISIT_FP8_QK = 3 };
 
 /* Correspondence reason codes written to out_idx by reproject_correspondence
- * (the rejection causes of Sec. 4.3, design choice (iii), plus an empty
- * retrieved slot). A value >= 0 is a key index within the source frame. */
+ * and reproject_rotation (the rejection causes of Sec. 4.3, design choice
+ * (iii), plus an empty retrieved slot and, for the rotation-only path, a
+ * source whose centre is not the target's). A value >= 0 is a key index
+ * within the source frame. */
 enum {
     REVISIT_UNDEFINED = -1, /* query depth not finite or <= 0 */
     REVISIT_BEHIND = -2,    /* [X_s]_z <= 0 */
     REVISIT_OFF_GRID = -3,  /* u^ outside [0, w) x [0, h) */
     REVISIT_OCCLUDED = -4,  /* Eq. visibility fails (or source depth NaN) */
-    REVISIT_NO_SOURCE = -5  /* the retrieved slot is empty */
+    REVISIT_NO_SOURCE = -5, /* the retrieved slot is empty */
+    REVISIT_CENTRE_MOVED = -6 /* reproject_rotation only: c_s != c_t */
 };
 
 /* Largest k accepted by retrieve_chunks. */
@@ -281,6 +287,42 @@ int pack_retrieved_kv(const void* store_k, const void* store_v,
                       int32_t F, int32_t h, int32_t w, int32_t H, int32_t D,
                       int32_t rope_t_pairs, float rope_theta,
                       hipStream_t stream);
+
+/*
+ * reproject_rotation -- Sec. 4.3, the fixed-centre case of Eq. reprojection.
+ *
+ * For sources that share the target's camera centre (c_s = c_t) the depth
+ * scales X_s and cancels under pi, so u^ = pi(K_s R_s^T R_t K_t^-1 u~) is a
+ * homography per (target, source) frame pair, independent of depth. This
+ * entry point evaluates it without reading any depth: the visibility test of
+ * Eq. visibility is not applied (one centre means no parallax and so no
+ * disocclusion), and REVISIT_UNDEFINED and REVISIT_OCCLUDED never occur.
+ * Per pair, in double:
+ *     A = R_s^T R_t,  A[r][c] = (Rs[0][r] Rt[0][c] + Rs[1][r] Rt[1][c]) + Rs[2][r] Rt[2][c]
+ *     M = K_s A,      rows (fx_s A0 + cx_s A2, fy_s A1 + cy_s A2, A2)
+ *     H = M K_t^-1,   H[r] = (M[r][0] / fx_t, M[r][1] / fy_t,
+ *                             (M[r][2] - H[r][0] cx_t) - H[r][1] cy_t)
+ * (token-grid intrinsics, i.e. divided by p), then per token
+ *     v = H (u_x, u_y, 1),  REVISIT_BEHIND iff v_z <= 0,  u^ = (v_x / v_z, v_y / v_z)
+ * with the grid test and key index of reproject_correspondence; no
+ * contraction, so the results are reproducible bit for bit. A pair whose fp32
+ * centres (the last pose column) are not equal is written as
+ * REVISIT_CENTRE_MOVED for every token, u^ NaN.
+ *
+ *   tgt_c2w [B][Tq][4][4], tgt_K [B][Tq][4] fp32;
+ *   sources src_c2w, src_K ([B][S][..], or a frame bank [n_src][..] chosen by
+ *   src_sel [B][S]) exactly as for reproject_correspondence;
+ *   h, w token grid; p >= 1 latent pixels per token side (intrinsics are in
+ *   depth-map pixels, as everywhere);
+ *   out_uv [B][S][Tq*h*w][2] fp32 (NaN for BEHIND, NO_SOURCE, CENTRE_MOVED),
+ *   out_idx [B][S][Tq*h*w] int32.
+ * Any of B, Tq, S equal to 0 is valid (nothing to do); S <= 64; out_uv must
+ * be 8-byte aligned (REVISIT_ERR_SHAPE otherwise).
+ */
+int reproject_rotation(const float* tgt_c2w, const float* tgt_K, const float* src_c2w, const float* src_K,
+                       const int32_t* src_sel, int32_t n_src, int32_t B, int32_t Tq, int32_t S,
+                       int32_t h, int32_t w, int32_t p, float* out_uv, int32_t* out_idx,
+                       hipStream_t stream);
 
 /*
  * pool_token_depth -- the query and source depth of Sec. 4.3 at token

@@ -3,11 +3,13 @@
 
 Python binding of librevisit: argument marshalling only. Every stage runs
 in the library's HIP kernels; torch tensors supply device memory and the
-current HIP stream. The three entry points mirror include/revisit.h:
+current HIP stream. The entry points mirror include/revisit.h:
 
 * ``retrieve_chunks``          -- pose retrieval (Sec. 4.2, Eq. retrieval)
 * ``reproject_correspondence`` -- depth/pose reprojection and visibility
                                   (Sec. 4.3, Eq. reprojection, Eq. visibility)
+* ``reproject_rotation``       -- its fixed-centre case, the rotation / zoom
+                                  homography without depth (Sec. 4.3)
 * ``biased_chunk_attention``   -- attention with the Gaussian correspondence
                                   bias (Sec. 4.3, Eq. bias)
 
@@ -25,7 +27,7 @@ import torch
 from . import _lib
 from ._lib import BF16, F32, FP8_QK, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
 
-__all__ = ["retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "pack_retrieved_kv",
+__all__ = ["retrieve_chunks", "reproject_correspondence", "reproject_rotation", "biased_chunk_attention", "pack_retrieved_kv",
            "pool_token_depth", "StreamDriver", "set_attention_key_parts",
            "RevisitError", "lib"]
 
@@ -136,6 +138,56 @@ def reproject_correspondence(tgt_depth: torch.Tensor, tgt_c2w: torch.Tensor, tgt
                                         _ptr(src_c2w), _ptr(src_K), _ptr(src_sel), n_src, B, Tq, S, h, w, p,
                                         eps, _ptr(uv), _ptr(idx), _stream(dev))
     _lib.check("reproject_correspondence", st)
+    if not batched:
+        return uv[0], idx[0]
+    return uv, idx
+
+
+def reproject_rotation(tgt_c2w: torch.Tensor, tgt_K: torch.Tensor, src_c2w: torch.Tensor, src_K: torch.Tensor, *,
+                       h: int, w: int, p: int, src_sel: Optional[torch.Tensor] = None, out=None):
+    """Rotation-only correspondence (sources sharing the target's centre): the
+    homography u^ = pi(K_s R_s^T R_t K_t^-1 u~), no depth, no visibility test.
+
+    Batched: tgt_c2w [B,Tq,4,4], tgt_K [B,Tq,4]; sources [B,S,...] or, with
+    src_sel [B,S] i32, a frame bank [n_src,...]; h, w the token grid, p the
+    latent pixels per token side (K is in depth-map pixels). Unbatched inputs
+    give unbatched outputs. Returns (uv [B,S,Tq*h*w,2] f32, idx [B,S,Tq*h*w]
+    i32), idx = REVISIT_CENTRE_MOVED (-6) for a pair whose centres differ."""
+    batched = tgt_c2w.dim() == 4
+    if not batched:
+        tgt_c2w, tgt_K = tgt_c2w[None], tgt_K[None]
+        if src_sel is None:
+            src_c2w, src_K = src_c2w[None], src_K[None]
+        else:
+            src_sel = src_sel[None]
+    dev = tgt_c2w.device
+    if tgt_c2w.dim() != 4:
+        raise ValueError(f"tgt_c2w must be [B,Tq,4,4] or [Tq,4,4] (got {tuple(tgt_c2w.shape)})")
+    B, Tq = tgt_c2w.shape[:2]
+    _need(tgt_c2w, "tgt_c2w", torch.float32, (B, Tq, 4, 4), dev)
+    _need(tgt_K, "tgt_K", torch.float32, (B, Tq, 4), dev)
+    if src_sel is None:
+        S = src_c2w.shape[1]
+        _need(src_c2w, "src_c2w", torch.float32, (B, S, 4, 4), dev)
+        _need(src_K, "src_K", torch.float32, (B, S, 4), dev)
+        n_src = 0
+    else:
+        S = src_sel.shape[1]
+        n_src = src_c2w.shape[0]
+        _need(src_sel, "src_sel", torch.int32, (B, S), dev)
+        _need(src_c2w, "src_c2w", torch.float32, (n_src, 4, 4), dev)
+        _need(src_K, "src_K", torch.float32, (n_src, 4), dev)
+    Lq = Tq * h * w
+    if out is None:
+        uv = torch.empty((B, S, Lq, 2), dtype=torch.float32, device=dev)
+        idx = torch.empty((B, S, Lq), dtype=torch.int32, device=dev)
+    else:
+        uv, idx = out
+        _need(uv, "out uv", torch.float32, (B, S, Lq, 2), dev)
+        _need(idx, "out idx", torch.int32, (B, S, Lq), dev)
+    st = lib().reproject_rotation(_ptr(tgt_c2w), _ptr(tgt_K), _ptr(src_c2w), _ptr(src_K), _ptr(src_sel), n_src,
+                                  B, Tq, S, h, w, p, _ptr(uv), _ptr(idx), _stream(dev))
+    _lib.check("reproject_rotation", st)
     if not batched:
         return uv[0], idx[0]
     return uv, idx

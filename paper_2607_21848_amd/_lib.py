@@ -17,7 +17,7 @@ OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH, ERR_MEMORY = 0,
 BF16, F32, FP8_QK = 1, 2, 3
 MAX_K = 32
 EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
-            "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv", "pool_token_depth", "rc_stream_create",
+            "reproject_rotation", "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv", "pool_token_depth", "rc_stream_create",
             "rc_stream_step", "rc_stream_view", "rc_stream_destroy")
 
 _p = ctypes.c_void_p
@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
         L.reproject_correspondence.restype = ctypes.c_int
         L.reproject_correspondence.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _f,
                                                _p, _p, _p]
+        L.reproject_rotation.restype = ctypes.c_int
+        L.reproject_rotation.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p]
         L.biased_chunk_attention.restype = ctypes.c_int
         L.biased_chunk_attention.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _i,
                                              _f, _f, _f, _p]

@@ -167,6 +167,45 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
     return launched(revisit::launch_reproject(a, stream), "reproject_correspondence");
 }
 
+int reproject_rotation(const float* tgt_c2w, const float* tgt_K, const float* src_c2w, const float* src_K,
+                       const int32_t* src_sel, int32_t n_src, int32_t B, int32_t Tq, int32_t S, int32_t h, int32_t w,
+                       int32_t p, float* out_uv, int32_t* out_idx, hipStream_t stream) {
+    if (B < 0 || Tq < 0 || S < 0 || h < 1 || w < 1 || p < 1)
+        return fail(REVISIT_ERR_SHAPE, "reproject_rotation: need B, Tq, S >= 0 and h, w, p >= 1");
+    if ((int64_t)h * w > ((int64_t)1 << 28))
+        return fail(REVISIT_ERR_SHAPE, "reproject_rotation: frame too large");
+    if ((int64_t)B * Tq * h * w > ((int64_t)1 << 31) - 1 || (int64_t)B * S * Tq * h * w > kMaxElems)
+        return fail(REVISIT_ERR_SHAPE, "reproject_rotation: problem too large");
+    if (src_sel && n_src < 0) return fail(REVISIT_ERR_SHAPE, "reproject_rotation: n_src < 0");
+    if (S > 64) return fail(REVISIT_ERR_SHAPE, "reproject_rotation: more than 64 source frames per problem");
+    if (B == 0 || Tq == 0 || S == 0) return REVISIT_OK;
+    if (!tgt_c2w || !tgt_K || !out_uv || !out_idx)
+        return fail(REVISIT_ERR_NULL, "reproject_rotation: required pointer is NULL");
+    if ((!src_sel || n_src > 0) && (!src_c2w || !src_K))
+        return fail(REVISIT_ERR_NULL, "reproject_rotation: source pointer is NULL");
+    if (!aligned(out_uv, 8) || !aligned(out_idx, 4) || !aligned(src_sel, 4))
+        return fail(REVISIT_ERR_SHAPE, "reproject_rotation: out_uv must be 8-byte aligned, arrays 4-byte");
+    revisit::ReprojectArgs a;
+    a.tgt_depth = nullptr;
+    a.tgt_c2w = tgt_c2w;
+    a.tgt_K = tgt_K;
+    a.src_depth = nullptr;
+    a.src_c2w = src_c2w;
+    a.src_K = src_K;
+    a.src_sel = src_sel;
+    a.n_src = src_sel ? n_src : 0;
+    a.B = B;
+    a.Tq = Tq;
+    a.S = S;
+    a.h = h;
+    a.w = w;
+    a.p = p;
+    a.eps = 0.0;
+    a.out_uv = out_uv;
+    a.out_idx = out_idx;
+    return launched(revisit::launch_rotation(a, stream), "reproject_rotation");
+}
+
 int biased_chunk_attention(const void* q, const void* k, const void* v, void* o, float* lse, int32_t dtype,
                            int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
                            const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx, int32_t S,

@@ -60,6 +60,8 @@ struct ReprojectArgs {
     int32_t* out_idx;
 };
 hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream);
+// rotation-only correspondence: ReprojectArgs with the depth maps and eps unused
+hipError_t launch_rotation(const ReprojectArgs& a, hipStream_t stream);
 
 struct AttentionArgs {
     const void* q;

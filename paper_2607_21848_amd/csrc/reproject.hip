@@ -212,6 +212,110 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     }
 }
 
+// Rotation-only path (Sec. 4.3: with c_s = c_t the depth cancels in Eq.
+// reprojection, leaving the homography u^ = pi(K_s R_s^T R_t K_t^-1 u~)).
+// No depth is read and no visibility test applies. The block forms, per
+// source frame, H = (K_s (R_s^T R_t)) K_t^-1 in double in LDS, in the order
+//     A[r][c] = (Rs[0][r] Rt[0][c] + Rs[1][r] Rt[1][c]) + Rs[2][r] Rt[2][c]
+//     M = rows (fx_s A0 + cx_s A2, fy_s A1 + cy_s A2, A2)
+//     H[r] = (M[r][0] / fx_t, M[r][1] / fy_t, (M[r][2] - H[r][0] cx_t) - H[r][1] cy_t)
+// and each thread evaluates v = H u~ for its token, so the launch is a pure
+// write stream of 12 bytes per (token, source).
+struct SrcHomographies {
+    double H[kMaxSrcLds][9];
+    int status[kMaxSrcLds];  // 0 = use H, else the code of every token (-5, -6)
+};
+
+template <int P>
+__global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
+    const int hw = a.h * a.w;
+    const int blocks_per_frame = (hw + kBlock - 1) / kBlock;
+    const unsigned n_items = (unsigned)(blocks_per_frame * a.B * a.Tq);
+    const int item = (int)__builtin_amdgcn_readfirstlane(xcd_item(blockIdx.x, n_items));
+    if (item >= (int)n_items) return;  // grid padding (uniform, before the barrier)
+    const int bt = __builtin_amdgcn_readfirstlane(item / blocks_per_frame);  // b * Tq + t
+    const int b = __builtin_amdgcn_readfirstlane(bt / a.Tq);
+    const int t = bt - b * a.Tq;
+    const int tok = (item - bt * blocks_per_frame) * kBlock + threadIdx.x;
+    const int Lq = a.Tq * hw;
+    const double pd = (double)(P > 0 ? P : a.p);
+
+    __shared__ SrcHomographies sh;
+    for (int s = threadIdx.x; s < a.S; s += kBlock) {
+        int f = b * a.S + s;
+        if (a.src_sel) {
+            f = a.src_sel[(size_t)b * a.S + s];
+            if (f < 0 || f >= a.n_src) f = -1;
+        }
+        int status = 0;
+        if (f < 0) {
+            status = -5;
+        } else {
+            const float* Mt = a.tgt_c2w + (size_t)bt * 16;
+            const float* Ms = a.src_c2w + (size_t)f * 16;
+            if (!(Mt[3] == Ms[3] && Mt[7] == Ms[7] && Mt[11] == Ms[11])) {
+                status = -6;
+            } else {
+                const float* Kt = a.tgt_K + (size_t)bt * 4;
+                const float* Ks = a.src_K + (size_t)f * 4;
+                const double fxt = per_token<P>(Kt[0], pd), fyt = per_token<P>(Kt[1], pd);
+                const double cxt = per_token<P>(Kt[2], pd), cyt = per_token<P>(Kt[3], pd);
+                const double fxs = per_token<P>(Ks[0], pd), fys = per_token<P>(Ks[1], pd);
+                const double cxs = per_token<P>(Ks[2], pd), cys = per_token<P>(Ks[3], pd);
+                double A[3][3];
+                for (int r = 0; r < 3; ++r)
+                    for (int c = 0; c < 3; ++c)
+                        A[r][c] = ((double)Ms[r] * (double)Mt[c] + (double)Ms[4 + r] * (double)Mt[4 + c]) +
+                                  (double)Ms[8 + r] * (double)Mt[8 + c];
+                for (int c = 0; c < 3; ++c) {
+                    const double m0 = fxs * A[0][c] + cxs * A[2][c];
+                    const double m1 = fys * A[1][c] + cys * A[2][c];
+                    const double m2 = A[2][c];
+                    A[0][c] = m0;
+                    A[1][c] = m1;
+                    A[2][c] = m2;
+                }
+                for (int r = 0; r < 3; ++r) {
+                    const double h0 = A[r][0] / fxt;
+                    const double h1 = A[r][1] / fyt;
+                    sh.H[s][3 * r + 0] = h0;
+                    sh.H[s][3 * r + 1] = h1;
+                    sh.H[s][3 * r + 2] = (A[r][2] - h0 * cxt) - h1 * cyt;
+                }
+            }
+        }
+        sh.status[s] = status;
+    }
+    __syncthreads();
+    if (tok >= hw) return;
+    const int i = tok / a.w;
+    const int j = tok - i * a.w;
+    const double ux = (double)j + 0.5, uy = (double)i + 0.5;
+    for (int s = 0; s < a.S; ++s) {
+        const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
+        float2 uv = make_float2(NAN, NAN);
+        int code = sh.status[s];
+        if (code == 0) {
+            const double* H = sh.H[s];
+            const double v0 = (H[0] * ux + H[1] * uy) + H[2];
+            const double v1 = (H[3] * ux + H[4] * uy) + H[5];
+            const double v2 = (H[6] * ux + H[7] * uy) + H[8];
+            if (!(v2 > 0.0)) {
+                code = -2;
+            } else {
+                const double uhx = v0 / v2;
+                const double uhy = v1 / v2;
+                uv = make_float2((float)uhx, (float)uhy);
+                code = (uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h)
+                           ? (int)floor(uhy) * a.w + (int)floor(uhx)
+                           : -3;
+            }
+        }
+        st_uv(reinterpret_cast<float2*>(a.out_uv) + o, uv);
+        st_code(a.out_idx + o, code);
+    }
+}
+
 }  // namespace
 
 template <bool kPerSource>
@@ -237,6 +341,18 @@ hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream) {
     const dim3 grid(xcd_grid((unsigned)grid_blocks));
     if (per_source) launch_p<true>(a, grid, stream);
     else launch_p<false>(a, grid, stream);
+    return hipGetLastError();
+}
+
+hipError_t launch_rotation(const ReprojectArgs& a, hipStream_t stream) {
+    const int hw = a.h * a.w;
+    if (a.B == 0 || a.Tq == 0 || a.S == 0 || hw == 0) return hipSuccess;
+    const int64_t blocks = (int64_t)((hw + kBlock - 1) / kBlock) * a.B * a.Tq;
+    if (blocks > INT32_MAX - kXcds) return hipErrorInvalidValue;
+    const dim3 grid(xcd_grid((unsigned)blocks)), block(kBlock);
+    if (a.p == 2) hipLaunchKernelGGL((rotation_kernel<2>), grid, block, 0, stream, a);
+    else if (a.p == 1) hipLaunchKernelGGL((rotation_kernel<1>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((rotation_kernel<0>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 

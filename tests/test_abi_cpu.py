@@ -29,7 +29,8 @@ def declared_functions():
 
 def test_header_declares_the_three_stages():
     names = declared_functions()
-    for n in ("retrieve_chunks", "reproject_correspondence", "biased_chunk_attention", "pack_retrieved_kv",
+    for n in ("retrieve_chunks", "reproject_correspondence", "reproject_rotation", "biased_chunk_attention",
+              "pack_retrieved_kv",
               "rc_status_string", "rc_last_error", "rc_set_attention_key_parts"):
         assert n in names
 
@@ -101,6 +102,33 @@ def test_reproject_rejects(L, kw, status):
 def test_reproject_empty_is_ok(L):
     assert _reproject(L, S=0, td=NULL, uv=NULL) == 0
     assert _reproject(L, B=0, td=NULL, uv=NULL) == 0
+
+
+def _rotation(L, **kw):
+    a = dict(tc=FAKE, tk=FAKE, sc=FAKE, sk=FAKE, sel=NULL, n_src=0, B=1, Tq=3, S=6, h=30, w=52, p=2, uv=FAKE,
+             idx=FAKE)
+    a.update(kw)
+    return L.reproject_rotation(a["tc"], a["tk"], a["sc"], a["sk"], a["sel"], a["n_src"], a["B"], a["Tq"], a["S"],
+                                a["h"], a["w"], a["p"], a["uv"], a["idx"], NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(h=0), 2), (dict(w=-3), 2), (dict(p=0), 2), (dict(B=-1), 2), (dict(Tq=-1), 2), (dict(S=65), 2),
+    (dict(tc=NULL), 1), (dict(tk=NULL), 1), (dict(uv=NULL), 1), (dict(idx=NULL), 1), (dict(sc=NULL), 1),
+    (dict(sel=FAKE, n_src=-1), 2), (dict(h=1 << 15, w=1 << 14), 2), (dict(B=1 << 20, h=64, w=64), 2),
+    (dict(uv=ctypes.c_void_p(0x1004)), 2),
+])
+def test_rotation_rejects(L, kw, status):
+    from paper_2607_21848_amd import _lib
+    assert _rotation(L, **kw) == status
+    assert "reproject_rotation" in _lib.last_error()
+
+
+def test_rotation_empty_is_ok(L):
+    assert _rotation(L, S=0, tc=NULL, uv=NULL) == 0
+    assert _rotation(L, B=0, tc=NULL, uv=NULL) == 0
+    # a bank with no frames needs no source pointers (every slot is empty)
+    assert _rotation(L, B=0, sel=FAKE, n_src=0, sc=NULL, sk=NULL) == 0
 
 
 def _attention(L, **kw):

@@ -1,0 +1,125 @@
+"""GPU parity of reproject_rotation (Sec. 4.3, the fixed-centre homography)
+against the oracle: codes and u^ bit for bit (both sides evaluate the same
+IEEE double expressions and round u^ to fp32 once).
+
+Cases: the panorama-clip workload at the 30 x 52 grid; ragged grids at
+p = 1, 2, 3 spanning several 128-token blocks with a partial last one; a
+source with a moved centre (code -6); a frame bank with empty and
+out-of-range selections (-5); the full 1024-problem launch the benchmark
+times, checked on sampled problems; and agreement with the general kernel
+(reproject_correspondence) on shared-centre inputs, where depth cancels.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_21848_amd as rv
+import workloads as W
+from oracle import reprojection as R
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rv.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _d(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _check(uv, idx, want_uv, want_idx):
+    assert np.array_equal(idx, want_idx)
+    assert np.array_equal(uv.view(np.uint32), want_uv.view(np.uint32))
+
+
+def test_rotation_panorama_clips():
+    tc, tk, sc, sk = W.make_rotation_batch(6)
+    print("reproject_rotation: panorama clips B=6 30x52 p=2", flush=True)
+    uv, idx = rv.reproject_rotation(_d(tc), _d(tk), _d(sc), _d(sk), h=30, w=52, p=2)
+    uv, idx = uv.cpu().numpy(), idx.cpu().numpy()
+    for b in range(6):
+        wu, wi = R.reproject_rotation(tc[b], tk[b], sc[b], sk[b], 30, 52, 2)
+        _check(uv[b], idx[b], wu, wi)
+    assert (idx >= 0).mean() > 0.4 and (idx == R.OFF_GRID).any() and (idx == R.BEHIND).any()
+
+
+@pytest.mark.parametrize("h,w,p", [(7, 13, 1), (11, 29, 2), (9, 31, 3), (1, 1, 2)])
+def test_rotation_ragged_grids_and_moved_centre(h, w, p):
+    tc, tk, sc, sk = W.make_rotation_batch(3, Tq=2, S=5, h=h, w=w, p=p, distinct=3, seed=77 + p)
+    sc = sc.copy()
+    sc[1, 2, 0, 3] += np.float32(1e-3)  # one source of problem 1 leaves the centre
+    print(f"reproject_rotation: ragged h={h} w={w} p={p}", flush=True)
+    uv, idx = rv.reproject_rotation(_d(tc), _d(tk), _d(sc), _d(sk), h=h, w=w, p=p)
+    uv, idx = uv.cpu().numpy(), idx.cpu().numpy()
+    for b in range(3):
+        wu, wi = R.reproject_rotation(tc[b], tk[b], sc[b], sk[b], h, w, p)
+        _check(uv[b], idx[b], wu, wi)
+    assert np.all(idx[1, 2] == R.CENTRE_MOVED) and np.all(np.isnan(uv[1, 2]))
+
+
+def test_rotation_frame_bank_selection():
+    tc, tk, sc, sk = W.make_rotation_batch(4, S=6, distinct=4, seed=91)
+    bank_c2w = sc.reshape(-1, 4, 4)
+    bank_K = sk.reshape(-1, 4)
+    sel = np.arange(24, dtype=np.int32).reshape(4, 6)
+    sel[0, 1] = -1
+    sel[2, 5] = 24  # outside the bank: no source
+    sel[3, 0] = 2   # another problem's frame: another centre
+    print("reproject_rotation: frame bank 24 frames, B=4", flush=True)
+    uv, idx = rv.reproject_rotation(_d(tc), _d(tk), _d(bank_c2w), _d(bank_K), h=30, w=52, p=2, src_sel=_d(sel))
+    uv, idx = uv.cpu().numpy(), idx.cpu().numpy()
+    for b in range(4):
+        wu, wi = R.reproject_rotation(tc[b], tk[b], bank_c2w, bank_K, 30, 52, 2, src_sel=sel[b])
+        _check(uv[b], idx[b], wu, wi)
+    assert np.all(idx[0, 1] == R.NO_SOURCE) and np.all(idx[2, 5] == R.NO_SOURCE)
+    assert np.all(idx[3, 0] == R.CENTRE_MOVED)
+
+
+def test_rotation_full_batch_sampled():
+    """The 1024-problem launch of the benchmark; 16 distinct problems tiled,
+    so checking every distinct one (at its first and last copy) covers all."""
+    tc, tk, sc, sk = W.make_rotation_batch(1024)
+    print("reproject_rotation: B=1024 30x52 p=2", flush=True)
+    uv, idx = rv.reproject_rotation(_d(tc), _d(tk), _d(sc), _d(sk), h=30, w=52, p=2)
+    torch.cuda.synchronize()
+    for b in list(range(16)) + list(range(1008, 1024)):
+        wu, wi = R.reproject_rotation(tc[b], tk[b], sc[b], sk[b], 30, 52, 2)
+        _check(uv[b].cpu().numpy(), idx[b].cpu().numpy(), wu, wi)
+
+
+def test_rotation_empty_batch():
+    tc = torch.zeros((0, 3, 4, 4), device="cuda")
+    tk = torch.zeros((0, 3, 4), device="cuda")
+    uv, idx = rv.reproject_rotation(tc, tk, torch.zeros((0, 6, 4, 4), device="cuda"),
+                                    torch.zeros((0, 6, 4), device="cuda"), h=30, w=52, p=2)
+    assert uv.shape == (0, 6, 4680, 2) and idx.shape == (0, 6, 4680)
+
+
+def test_rotation_agrees_with_the_general_kernel():
+    """Shared centres and positive depth through reproject_correspondence:
+    u^ agrees to rounding, and every code the depth test did not decide
+    agrees exactly (tokens within 1e-4 px of a cell boundary excepted)."""
+    tc, tk, sc, sk = W.make_rotation_batch(8, distinct=8, seed=5)
+    rng = np.random.default_rng(3)
+    td = rng.uniform(0.5, 50.0, (8, 3, 60, 104)).astype(np.float32)
+    sd = rng.uniform(0.5, 50.0, (8, 6, 60, 104)).astype(np.float32)
+    print("reproject_rotation vs reproject_correspondence: B=8", flush=True)
+    uv_g, idx_g = rv.reproject_correspondence(_d(td), _d(tc), _d(tk), _d(sd), _d(sc), _d(sk), p=2, eps=0.05)
+    uv_r, idx_r = rv.reproject_rotation(_d(tc), _d(tk), _d(sc), _d(sk), h=30, w=52, p=2)
+    uv_g, idx_g, uv_r, idx_r = (x.cpu().numpy() for x in (uv_g, idx_g, uv_r, idx_r))
+    front = idx_g != R.BEHIND
+    assert np.array_equal(idx_r == R.BEHIND, ~front)
+    scale = np.maximum(1.0, np.abs(uv_g[front]).astype(np.float64))
+    assert np.all(np.abs(uv_r[front] - uv_g[front]) <= 1e-5 * scale)
+    far = front & (R.boundary_margin(uv_g, 2, 30, 52) > 1e-4) & (idx_g != R.OCCLUDED)
+    assert far.mean() > 0.3
+    assert np.array_equal(idx_r[far], idx_g[far])

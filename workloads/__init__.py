@@ -22,5 +22,6 @@ from .configs import (  # noqa: F401
     make_c4,
     make_c5,
     make_reproj_batch,
+    make_rotation_batch,
 )
 from .synth import bf16_round, bf16_bits, look_pose, perturb_pose  # noqa: F401

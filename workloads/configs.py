@@ -259,6 +259,49 @@ def make_reproj_batch(B: int, distinct: int = 16, seed: int = 3003):
                  for i in range(6))
 
 
+def _fov_K(fov_deg: float, H: int, W: int) -> np.ndarray:
+    """Pinhole (fx, fy, cx, cy) in depth-map pixels for a horizontal FOV."""
+    f = (W / 2.0) / np.tan(np.deg2rad(fov_deg) / 2.0)
+    return np.array([f, f, W / 2.0, H / 2.0])
+
+
+def make_rotation_batch(B: int, Tq: int = 3, S: int = 6, h: int = 30, w: int = 52, p: int = 2,
+                        distinct: int = 16, seed: int = 3006):
+    """B shared-centre problems shaped like the paper's panorama-rendered
+    revisit clips (Sec. 5: a rotation excursion that yaws away by 90-180
+    degrees and returns, or a zoom excursion from a 90 to a 35 degree FOV and
+    back). Per problem one camera centre; the S source frames are the
+    outward leg, the Tq target frames the return leg near the same headings
+    (+-10 degrees yaw, +-3 degrees pitch jitter). Even problems rotate at a
+    90 degree FOV, odd ones zoom at a fixed heading. ``distinct`` problems are
+    generated and tiled to B. Returns tgt_c2w [B,Tq,4,4], tgt_K [B,Tq,4],
+    src_c2w [B,S,4,4], src_K [B,S,4], all fp32."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    H, W = h * p, w * p
+    probs = []
+    for n in range(min(B, distinct)):
+        c = rng.uniform(-20.0, 20.0, 3)
+        c[2] = rng.uniform(1.0, 3.0)
+        yaw0 = rng.uniform(0.0, 2 * np.pi)
+        if n % 2 == 0:
+            span = np.deg2rad(rng.uniform(90.0, 180.0))
+            yaws = yaw0 + span * np.arange(S) / max(S - 1, 1)
+            fovs = np.full(S, 90.0)
+        else:
+            yaws = np.full(S, yaw0)
+            fovs = 90.0 - (90.0 - 35.0) * np.arange(S) / max(S - 1, 1)
+        src_c2w = np.stack([look_pose(c, yaw=y, pitch=0.05) for y in yaws])
+        src_K = np.stack([_fov_K(f, H, W) for f in fovs])
+        pick = rng.integers(0, S, Tq)
+        tgt_c2w = np.stack([look_pose(c, yaw=yaws[k] + np.deg2rad(rng.uniform(-10, 10)),
+                                      pitch=0.05 + np.deg2rad(rng.uniform(-3, 3))) for k in pick])
+        tgt_K = np.stack([_fov_K(fovs[k] * rng.uniform(0.95, 1.05), H, W) for k in pick])
+        probs.append(tuple(x.astype(np.float32) for x in (tgt_c2w, tgt_K, src_c2w, src_K)))
+    reps = -(-B // len(probs))
+    return tuple(np.ascontiguousarray(np.concatenate([np.stack([pr[i] for pr in probs])] * reps)[:B])
+                 for i in range(4))
+
+
 # --------------------------------------------------------------------------
 # C4 / C5: history bank on a loop + retrieval
 # --------------------------------------------------------------------------
