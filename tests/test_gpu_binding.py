@@ -1,7 +1,8 @@
 """The Python binding rejects malformed device arguments before any launch:
-caller-supplied outputs of the wrong shape or dtype, and a KV-frame slot
-table whose length is not the number of KV frames (the kernels would read
-or write past those buffers)."""
+caller-supplied outputs of the wrong shape or dtype, a KV-frame slot table
+whose length is not the number of KV frames, and malformed poses or
+selections for the rotation-only call (the kernels would read or write past
+those buffers)."""
 
 from __future__ import annotations
 
@@ -58,3 +59,36 @@ def test_attention_rejects_slot_table_of_wrong_length():
     with pytest.raises(ValueError):  # Lk not a whole number of frames
         rv.biased_chunk_attention(q, k[:30], k[:30], torch.full((2,), -1, dtype=torch.int32, device=DEV), None, None,
                                   **kw)
+
+
+def test_rotation_binding_checks_and_unbatched_form():
+    """reproject_rotation: malformed poses, intrinsics, selections or outputs
+    raise before any launch; unbatched inputs give unbatched outputs equal to
+    the batched call's first problem."""
+    eye = torch.eye(4, dtype=torch.float32, device=DEV)
+    tc = eye.repeat(2, 3, 1, 1).contiguous()  # [B=2, Tq=3, 4, 4]
+    tk = torch.tensor([20.0, 20.0, 13.0, 9.0], device=DEV).repeat(2, 3, 1).contiguous()
+    sc, sk = tc[:, :2].contiguous(), tk[:, :2].contiguous()  # S = 2
+    kw = dict(h=9, w=13, p=2)
+    with pytest.raises(TypeError):
+        rv.reproject_rotation(tc.double(), tk, sc, sk, **kw)
+    with pytest.raises(ValueError):
+        rv.reproject_rotation(tc, tk[:, :2].contiguous(), sc, sk, **kw)
+    with pytest.raises(ValueError):  # non-contiguous poses
+        rv.reproject_rotation(tc.transpose(2, 3), tk, sc, sk, **kw)
+    with pytest.raises(ValueError):  # a frame bank with a selection of the wrong batch
+        rv.reproject_rotation(tc, tk, sc.reshape(4, 4, 4), sk.reshape(4, 4), **kw,
+                              src_sel=torch.zeros((3, 2), dtype=torch.int32, device=DEV))
+    with pytest.raises(ValueError):
+        rv.reproject_rotation(tc, tk, sc, sk, **kw, out=(torch.empty((2, 2, 351, 2), device=DEV),
+                                                        torch.empty((2, 2, 350), dtype=torch.int32, device=DEV)))
+    with pytest.raises(TypeError):
+        rv.reproject_rotation(tc, tk, sc, sk, **kw, out=(torch.empty((2, 2, 351, 2), device=DEV),
+                                                        torch.empty((2, 2, 351), device=DEV)))
+    uv, idx = rv.reproject_rotation(tc, tk, sc, sk, **kw)
+    uv1, idx1 = rv.reproject_rotation(tc[0], tk[0], sc[0], sk[0], **kw)
+    torch.cuda.synchronize()
+    assert idx1.shape == (2, 351) and torch.equal(idx1, idx[0])
+    assert torch.equal(uv1.view(torch.int32), uv[0].view(torch.int32))
+    # identity poses: every token of each of the 3 frames maps onto itself
+    assert torch.equal(idx[1, 0], torch.arange(117, dtype=torch.int32, device=DEV).repeat(3))
