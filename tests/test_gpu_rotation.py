@@ -6,7 +6,7 @@ Cases: the panorama-clip workload at the 30 x 52 grid; ragged grids at
 p = 1, 2, 3 spanning several 128-token blocks with a partial last one; a
 source with a moved centre (code -6); a frame bank with empty and
 out-of-range selections (-5); the full 1024-problem launch the benchmark
-times, checked on sampled problems; and agreement with the general kernel
+times, checked on sampled problems; S = 64 sources; and agreement with the general kernel
 (reproject_correspondence) on shared-centre inputs, where depth cancels.
 """
 
@@ -123,3 +123,16 @@ def test_rotation_agrees_with_the_general_kernel():
     far = front & (R.boundary_margin(uv_g, 2, 30, 52) > 1e-4) & (idx_g != R.OCCLUDED)
     assert far.mean() > 0.3
     assert np.array_equal(idx_r[far], idx_g[far])
+
+
+def test_rotation_maximum_source_count():
+    """S = 64, the largest source count (the block's homography table is
+    full), against the oracle."""
+    tc, tk, sc, sk = W.make_rotation_batch(2, Tq=1, S=64, h=5, w=7, p=2, distinct=2, seed=64)
+    print("reproject_rotation: S=64 5x7 p=2", flush=True)
+    uv, idx = rv.reproject_rotation(_d(tc), _d(tk), _d(sc), _d(sk), h=5, w=7, p=2)
+    uv, idx = uv.cpu().numpy(), idx.cpu().numpy()
+    for b in range(2):
+        wu, wi = R.reproject_rotation(tc[b], tk[b], sc[b], sk[b], 5, 7, 2)
+        _check(uv[b], idx[b], wu, wi)
+    assert (idx >= 0).any()
