@@ -219,8 +219,10 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
 //     A[r][c] = (Rs[0][r] Rt[0][c] + Rs[1][r] Rt[1][c]) + Rs[2][r] Rt[2][c]
 //     M = rows (fx_s A0 + cx_s A2, fy_s A1 + cy_s A2, A2)
 //     H[r] = (M[r][0] / fx_t, M[r][1] / fy_t, (M[r][2] - H[r][0] cx_t) - H[r][1] cy_t)
-// and each thread evaluates v = H u~ for its token, so the launch is a pure
-// write stream of 12 bytes per (token, source).
+// and each thread evaluates v = H u~ for two adjacent tokens, so the launch
+// is a pure write stream of 12 bytes per (token, source). The pair's u^ go
+// out as one 16-byte store and its codes as one 8-byte store where the pair
+// is aligned (the common case), else one token at a time.
 struct SrcHomographies {
     double H[kMaxSrcLds][9];
     int status[kMaxSrcLds];  // 0 = use H, else the code of every token (-5, -6)
@@ -229,14 +231,14 @@ struct SrcHomographies {
 template <int P>
 __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
     const int hw = a.h * a.w;
-    const int blocks_per_frame = (hw + kBlock - 1) / kBlock;
+    const int blocks_per_frame = (hw + 2 * kBlock - 1) / (2 * kBlock);
     const unsigned n_items = (unsigned)(blocks_per_frame * a.B * a.Tq);
     const int item = (int)__builtin_amdgcn_readfirstlane(xcd_item(blockIdx.x, n_items));
     if (item >= (int)n_items) return;  // grid padding (uniform, before the barrier)
     const int bt = __builtin_amdgcn_readfirstlane(item / blocks_per_frame);  // b * Tq + t
     const int b = __builtin_amdgcn_readfirstlane(bt / a.Tq);
     const int t = bt - b * a.Tq;
-    const int tok = (item - bt * blocks_per_frame) * kBlock + threadIdx.x;
+    const int tok = 2 * ((item - bt * blocks_per_frame) * kBlock + threadIdx.x);
     const int Lq = a.Tq * hw;
     const double pd = (double)(P > 0 ? P : a.p);
 
@@ -288,31 +290,53 @@ __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
     }
     __syncthreads();
     if (tok >= hw) return;
-    const int i = tok / a.w;
-    const int j = tok - i * a.w;
-    const double ux = (double)j + 0.5, uy = (double)i + 0.5;
+    const bool two = tok + 1 < hw;
+    int i0 = tok / a.w;
+    int j0 = tok - i0 * a.w;
+    int i1 = i0, j1 = j0 + 1;
+    if (j1 == a.w) { j1 = 0; i1 = i0 + 1; }
+    const double ux0 = (double)j0 + 0.5, uy0 = (double)i0 + 0.5;
+    const double ux1 = (double)j1 + 0.5, uy1 = (double)i1 + 0.5;
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    typedef int i2 __attribute__((ext_vector_type(2)));
+    // the pair's second token (past the frame when tok + 1 == hw: computed, not stored)
     for (int s = 0; s < a.S; ++s) {
         const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
-        float2 uv = make_float2(NAN, NAN);
-        int code = sh.status[s];
-        if (code == 0) {
+        float2 uv[2] = {make_float2(NAN, NAN), make_float2(NAN, NAN)};
+        int code[2] = {sh.status[s], sh.status[s]};
+        if (code[0] == 0) {
             const double* H = sh.H[s];
-            const double v0 = (H[0] * ux + H[1] * uy) + H[2];
-            const double v1 = (H[3] * ux + H[4] * uy) + H[5];
-            const double v2 = (H[6] * ux + H[7] * uy) + H[8];
-            if (!(v2 > 0.0)) {
-                code = -2;
-            } else {
-                const double uhx = v0 / v2;
-                const double uhy = v1 / v2;
-                uv = make_float2((float)uhx, (float)uhy);
-                code = (uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h)
-                           ? (int)floor(uhy) * a.w + (int)floor(uhx)
-                           : -3;
+#pragma unroll
+            for (int g = 0; g < 2; ++g) {
+                const double ux = g ? ux1 : ux0, uy = g ? uy1 : uy0;
+                const double v0 = (H[0] * ux + H[1] * uy) + H[2];
+                const double v1 = (H[3] * ux + H[4] * uy) + H[5];
+                const double v2 = (H[6] * ux + H[7] * uy) + H[8];
+                if (!(v2 > 0.0)) {
+                    code[g] = -2;
+                } else {
+                    const double uhx = v0 / v2;
+                    const double uhy = v1 / v2;
+                    uv[g] = make_float2((float)uhx, (float)uhy);
+                    code[g] = (uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h)
+                                  ? (int)floor(uhy) * a.w + (int)floor(uhx)
+                                  : -3;
+                }
             }
         }
-        st_uv(reinterpret_cast<float2*>(a.out_uv) + o, uv);
-        st_code(a.out_idx + o, code);
+        if (two && (o & 1) == 0) {
+            f4 v = {uv[0].x, uv[0].y, uv[1].x, uv[1].y};
+            __builtin_nontemporal_store(v, reinterpret_cast<f4*>(a.out_uv + 2 * o));
+            i2 c = {code[0], code[1]};
+            __builtin_nontemporal_store(c, reinterpret_cast<i2*>(a.out_idx + o));
+        } else {
+            st_uv(reinterpret_cast<float2*>(a.out_uv) + o, uv[0]);
+            st_code(a.out_idx + o, code[0]);
+            if (two) {
+                st_uv(reinterpret_cast<float2*>(a.out_uv) + o + 1, uv[1]);
+                st_code(a.out_idx + o + 1, code[1]);
+            }
+        }
     }
 }
 
@@ -347,7 +371,7 @@ hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream) {
 hipError_t launch_rotation(const ReprojectArgs& a, hipStream_t stream) {
     const int hw = a.h * a.w;
     if (a.B == 0 || a.Tq == 0 || a.S == 0 || hw == 0) return hipSuccess;
-    const int64_t blocks = (int64_t)((hw + kBlock - 1) / kBlock) * a.B * a.Tq;
+    const int64_t blocks = (int64_t)((hw + 2 * kBlock - 1) / (2 * kBlock)) * a.B * a.Tq;
     if (blocks > INT32_MAX - kXcds) return hipErrorInvalidValue;
     const dim3 grid(xcd_grid((unsigned)blocks)), block(kBlock);
     if (a.p == 2) hipLaunchKernelGGL((rotation_kernel<2>), grid, block, 0, stream, a);
