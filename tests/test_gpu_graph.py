@@ -6,7 +6,8 @@ stream's workspace exists (a warm-up call on the capture stream creates
 it), so the three calls capture as kernel nodes. Every replay, with eager
 work of the library's on another stream between replays, must reproduce the
 eager results bit for bit: retrieval ids, scores, counts and frame
-selection, the correspondence map, and attention output and LSE."""
+selection, the correspondence map, and attention output and LSE. The
+rotation-only correspondence call is captured and replayed the same way."""
 
 from __future__ import annotations
 
@@ -70,3 +71,35 @@ def test_stage_path_replays_in_a_graph():
             assert torch.equal(buf[name], ref[name]), f"replay {rep}: {name} differs from the eager result"
         assert torch.equal(other["o"], ref["o"])
     print(f"graph of the stage path replayed 3 times, bit-identical to eager; retrieval {ref['ridx'].tolist()}")
+
+
+def test_rotation_only_correspondence_replays_in_a_graph():
+    """reproject_rotation allocates nothing and synchronises with nothing, so
+    it captures as one kernel node; every replay reproduces the eager map."""
+    dev = torch.device("cuda:0")
+    args = [torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in W.make_rotation_batch(64)]
+    shape = dict(h=30, w=52, p=2)
+
+    def outputs():
+        return (torch.empty((64, 6, 4680, 2), dtype=torch.float32, device=dev),
+                torch.empty((64, 6, 4680), dtype=torch.int32, device=dev))
+
+    cap = torch.cuda.Stream(dev)
+    ref, buf, other = outputs(), outputs(), outputs()
+    cap.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(cap):
+        rv.reproject_rotation(*args, **shape, out=ref)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cap):
+        rv.reproject_rotation(*args, **shape, out=buf)
+    for rep in range(3):
+        for x in buf:
+            x.zero_()
+        rv.reproject_rotation(*args, **shape, out=other)  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(buf[1], ref[1]), f"replay {rep}: codes differ from the eager result"
+        assert torch.equal(buf[0].view(torch.int32), ref[0].view(torch.int32)), f"replay {rep}: u^ differs"
+    assert (ref[1] >= 0).float().mean().item() > 0.4
