@@ -113,8 +113,8 @@ def main():
                          "kernel for scaling HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the path shards "
-              "per head / per query token across GPUs by design, but no multi-GPU run is part of it", flush=True)
+        print(f"bench.py: the benchmark runs on one GPU only (asked for --gpus {args.gpus}); the path would "
+              "shard per head and per query token across GPUs, but no multi-GPU path is implemented", flush=True)
         sys.exit(2)
 
     import torch
