@@ -76,3 +76,23 @@ def test_fp8e4m3_encoding_matches_torch():
                        [np.array([0.0, -0.0, 448.0, -448.0, 2.0**-9, 2.0**-10, 3 * 2.0**-10, -1e-5], np.float32)])
     want = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
     assert np.array_equal(fp8e4m3_bits(x), want)
+
+
+def test_rotation_batch_reproducible_and_shared_centres():
+    a, b = W.make_rotation_batch(20), W.make_rotation_batch(20)
+    for x, y in zip(a, b):
+        assert x.dtype == np.float32 and np.array_equal(x, y)
+    tc, tk, sc, sk = a
+    assert tc.shape == (20, 3, 4, 4) and tk.shape == (20, 3, 4) and sc.shape == (20, 6, 4, 4) and sk.shape == (20, 6, 4)
+    # one camera centre per problem, exactly (in fp32)
+    centres = np.concatenate([tc[:, :, :3, 3], sc[:, :, :3, 3]], axis=1)
+    assert np.array_equal(centres, np.broadcast_to(centres[:, :1], centres.shape))
+    # 16 distinct problems tiled to 20
+    assert np.array_equal(tc[16:], tc[:4]) and not np.array_equal(tc[1], tc[0])
+    # horizontal FOV of the sources: 90 degrees for rotation clips, 90 down to 35 for zoom clips
+    fov = np.degrees(2 * np.arctan((104 / 2) / sk[..., 0].astype(np.float64)))
+    assert np.allclose(fov[0::2], 90.0, atol=1e-3)
+    assert np.allclose(fov[1::2, 0], 90.0, atol=1e-3) and np.allclose(fov[1::2, -1], 35.0, atol=1e-3)
+    # the oracle finds the mix of outcomes the recipe states
+    _, idx = R.reproject_rotation(tc[0], tk[0], sc[0], sk[0], 30, 52, 2)
+    assert (idx >= 0).mean() > 0.3 and (idx == R.CENTRE_MOVED).sum() == 0
