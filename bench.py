@@ -154,6 +154,10 @@ def main():
     cidx = torch.empty((1, wl.S, wl.Lq), dtype=torch.int32, device=dev)
     o = torch.empty_like(q)
     lse = torch.empty((wl.H, wl.Lq), dtype=torch.float32, device=dev)
+    # the attention's key-split workspace (the library allocates nothing)
+    ws = torch.empty(max(rv.attention_workspace_size(torch.bfloat16, wl.Lq, wl.Lk, wl.H, wl.D),
+                         rv.attention_workspace_size(torch.float8_e4m3fn, wl.Lq, wl.Lk, wl.H, wl.D), 16),
+                     dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     def step(ev=None):
@@ -169,7 +173,7 @@ def main():
         if ev is not None:
             ev[2].record(stream)
         rv.biased_chunk_attention(q, k, v, slot, cuv[0], cidx[0], h=wl.h, w=wl.w, softmax_scale=wl.softmax_scale,
-                                  lam=wl.lam, sigma=wl.sigma, out=(o, lse))
+                                  lam=wl.lam, sigma=wl.sigma, out=(o, lse), workspace=ws)
         if ev is not None:
             ev[3].record(stream)
 
@@ -205,7 +209,7 @@ def main():
 
     def attn8():
         rv.biased_chunk_attention(q8, k8, v, slot, cuv[0], cidx[0], h=wl.h, w=wl.w, softmax_scale=wl.softmax_scale,
-                                  lam=wl.lam, sigma=wl.sigma, out=(o8, lse8))
+                                  lam=wl.lam, sigma=wl.sigma, out=(o8, lse8), workspace=ws)
     for _ in range(3):
         attn8()
     e8a, e8b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -308,13 +312,14 @@ def main():
     squery = torch.from_numpy(ring_bank(srng, 1, radius=20.0)).to(dev)
     schunk = torch.tensor([n_stress + 5], dtype=torch.int32, device=dev)
     sargs = dict(E=40.0, w_v=0.5, tau_c=0.05, tau_v=float(np.pi / 4), delta=3, first_candidate=1, k=4)
-    sout = rv.retrieve_chunks(sbank, squery, schunk, **sargs)
+    sws = torch.empty(max(rv.retrieve_workspace_size(n_stress, 1, sargs["k"]), 16), dtype=torch.uint8, device=dev)
+    sout = rv.retrieve_chunks(sbank, squery, schunk, **sargs, workspace=sws)
     for _ in range(3):
-        rv.retrieve_chunks(sbank, squery, schunk, **sargs, out=(*sout[:3], None))
+        rv.retrieve_chunks(sbank, squery, schunk, **sargs, out=(*sout[:3], None), workspace=sws)
     torch.cuda.synchronize()
     e0.record(stream)
     for _ in range(reps):
-        rv.retrieve_chunks(sbank, squery, schunk, **sargs, out=(*sout[:3], None))
+        rv.retrieve_chunks(sbank, squery, schunk, **sargs, out=(*sout[:3], None), workspace=sws)
     e1.record(stream)
     torch.cuda.synchronize()
     rs_ms = e0.elapsed_time(e1) / reps

@@ -29,15 +29,19 @@
  * --------------------------------------
  * - Every array argument is a DEVICE pointer owned by the caller and must
  *   stay valid until the work queued on `stream` has completed. Outputs must
- *   not alias inputs. State kept by the library: a per-thread last-error
- *   string, the setting of rc_set_attention_key_parts(), the per-stream
- *   workspace described at biased_chunk_attention (used by the bf16 key
- *   split and by the segmented retrieval of large banks), and the device
- *   memory of stream objects (rc_stream_create), which the caller owns
- *   through the handle.
- * - Calls are asynchronous on `stream` (NULL = the default stream).
+ *   not alias inputs. The stage calls allocate nothing and synchronise
+ *   nothing: where a kernel needs scratch memory (the key split of the bf16
+ *   attention, the segmented retrieval of large banks) the caller passes a
+ *   device workspace whose size the matching rc_*_workspace_size() query
+ *   returns. The only state kept by the library is a per-thread last-error
+ *   string; stream objects (rc_stream_create) own device memory that the
+ *   caller holds through the handle.
+ * - Calls are asynchronous on `stream` (NULL = the default stream). Work on
+ *   one workspace must not overlap in time: two calls that may run
+ *   concurrently (different streams) need different workspaces.
  * - Arguments are validated on the host before anything is queued: on a
- *   non-zero status nothing has been enqueued and rc_last_error() says why.
+ *   non-zero status nothing has been enqueued and rc_last_error() says why
+ *   (the one exception, rc_stream_step, is stated there).
  *   Device-resident index arrays (slots, selections) cannot be checked from
  *   the host; out-of-range entries there are given a defined meaning below
  *   instead of being read out of bounds.
@@ -52,6 +56,7 @@
 #ifndef REVISIT_H
 #define REVISIT_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -132,9 +137,13 @@ const char* rc_last_error(void);
  * otherwise). Banks of more than 8192 entries are scanned by many waves
  * (workgroups of 16 waves over segments of 16384 entries) whose k best
  * candidates are merged in the same (score, index) order, with the same
- * result; the segments' candidates go to the library-owned per-stream
- * workspace described at biased_chunk_attention (n_query * segments * k * 12
- * bytes).
+ * result; the segments' candidates go to the caller's workspace.
+ *
+ *   workspace, workspace_bytes  device scratch of at least the size
+ *                 rc_retrieve_workspace_size() returns for (n_bank, n_query,
+ *                 k), 16-byte aligned; may be NULL / 0 when that size is 0
+ *                 (banks of at most 8192 entries). Too small:
+ *                 REVISIT_ERR_SHAPE; NULL while needed: REVISIT_ERR_NULL.
  */
 int retrieve_chunks(const float* bank_c2w, int32_t n_bank,
                     const float* query_c2w, const int32_t* query_chunk, int32_t n_query,
@@ -142,7 +151,16 @@ int retrieve_chunks(const float* bank_c2w, int32_t n_bank,
                     int32_t delta, int32_t first_candidate, int32_t k,
                     int32_t* out_idx, float* out_score, int32_t* out_count,
                     int32_t frames_per_chunk, int32_t* out_frame_sel,
+                    void* workspace, size_t workspace_bytes,
                     hipStream_t stream);
+
+/*
+ * rc_retrieve_workspace_size -- bytes of workspace retrieve_chunks needs for
+ * a bank of n_bank entries, n_query queries and k results per query:
+ * n_query * segments * k * 12 with segments = ceil(n_bank / 16384) above
+ * 8192 entries, else 0. The arguments are validated as by retrieve_chunks.
+ */
+int rc_retrieve_workspace_size(int32_t n_bank, int32_t n_query, int32_t k, size_t* bytes);
 
 /*
  * reproject_correspondence -- Sec. 4.3, Eq. reprojection and Eq. visibility.
@@ -218,18 +236,34 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
  *
  * Lq == 0 is valid (nothing to do).
  *
+ * Bias precision. The fp32 path evaluates each bias term directly,
+ * -gamma ((u_k,x - u^_x)^2 + (u_k,y - u^_y)^2) with the differences taken
+ * first (gamma = lambda / (2 sigma^2 softmax_scale), in units of q . k), so
+ * its error is a few fp32 units of the term itself. The bf16 and fp8 paths add
+ * the bias on the matrix cores in separable form, 2 gamma a . u' - gamma |a|^2
+ * - gamma |u'|^2 with a, u' the key and query positions relative to the grid
+ * centre, each factor split exactly into bf16 pieces and summed in fp32: their
+ * absolute logit error is a few fp32 units (2^-24 relative) of
+ * lambda (|a|^2 + |u'|^2) / (2 sigma^2), which for in-grid u^ is at most
+ * lambda (h^2 + w^2) / (4 sigma^2): one unit is 1.3e-5 at sigma = 2 on a
+ * 30 x 52 grid and 8e-3 at sigma = 0.5 on 256 x 256.
+ *
  * bf16 work split: each (head, 128-query tile) item runs on one workgroup,
- * or, when the number of items leaves part of the GPU idle in the last round
- * of workgroups, its keys are cut into P equal parts that run on P
- * workgroups (P chosen per call, or set by rc_set_attention_key_parts()).
- * With P > 1 a second kernel on the same stream merges the parts from fp32
- * partial results in a library-owned device workspace (items * P * 66 KiB;
- * 234 MiB for 444 items in 8 parts): one block per (device, stream),
- * allocated with hipMalloc on the first call that needs it and grown by later
- * calls that need more (after synchronising that stream). Calls queued on one
- * stream share its block in order; calls on different streams never share
- * one. A failed allocation returns REVISIT_ERR_MEMORY (another HIP error
- * while getting the block, REVISIT_ERR_LAUNCH) with nothing enqueued.
+ * or its keys are cut into P equal parts that run on P workgroups, and a
+ * second kernel on the same stream merges the parts from fp32 partial
+ * results kept in the workspace.
+ *   key_parts   0 = P chosen from the shape and the compute units of the
+ *               current device (more parts when the items alone would leave
+ *               part of the GPU idle in the last round of workgroups), or a
+ *               fixed P in [1, 64] (clamped to the number of 32-key tiles).
+ *               Any P gives the same result up to the fp32 rounding of the
+ *               merge. fp32 ignores it.
+ *   workspace, workspace_bytes  device scratch of at least the size
+ *               rc_attention_workspace_size() returns for the same dtype,
+ *               shape and key_parts on the same device (items * P * 66.5 KiB
+ *               when P > 1, else 0), 16-byte aligned; may be NULL / 0 when
+ *               that size is 0. Too small: REVISIT_ERR_SHAPE; NULL while
+ *               needed: REVISIT_ERR_NULL.
  */
 int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
                            float* lse, int32_t dtype,
@@ -237,7 +271,17 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
                            const int32_t* kv_frame_slot,
                            const float* corr_uv, const int32_t* corr_idx, int32_t S,
                            float softmax_scale, float lambda, float sigma,
+                           int32_t key_parts, void* workspace, size_t workspace_bytes,
                            hipStream_t stream);
+
+/*
+ * rc_attention_workspace_size -- bytes of workspace biased_chunk_attention
+ * needs for this dtype, shape and key_parts on the current device (the
+ * automatic key_parts = 0 depends on its compute units). Shape and dtype are
+ * validated as by biased_chunk_attention.
+ */
+int rc_attention_workspace_size(int32_t dtype, int32_t Lq, int32_t Lk, int32_t H, int32_t D,
+                                int32_t key_parts, size_t* bytes);
 
 /*
  * pack_retrieved_kv -- Sec. 4.2, cache layout and cache packing.
@@ -380,6 +424,8 @@ int pool_token_depth(const float* depth, int32_t n_frames, int32_t h, int32_t w,
  *   Device memory: layers * capacity * F h w * H * D * 2 (K and V) elements
  *   for the ring plus layers * 5 F h w * H * D * 2 for the cache, plus small
  *   tables.
+ *   The object also owns the attention key-split and retrieval workspace of
+ *   its largest step, sized here for the current device.
  * rc_stream_step -- runs the next chunk. Inputs (device, caller-owned):
  *   depth [F][h p][w p] fp32 planar depth, c2w [F][4][4], K [F][4] depth-pixel
  *   intrinsics; q, k, v [layers][F h w][H][D] in dtype (k with the rotary
@@ -387,7 +433,13 @@ int pool_token_depth(const float* depth, int32_t n_frames, int32_t h, int32_t w,
  *   (nullable) [layers][H][F h w]. The device must be the one the stream was
  *   created on. Steps of one stream must be issued in order on one stream
  *   (they share the object's buffers); REVISIT_ERR_SHAPE once max_chunks
- *   chunks have run.
+ *   chunks have run. Every argument and the whole step's configuration are
+ *   validated before the first launch, so a status other than
+ *   REVISIT_ERR_LAUNCH means nothing was enqueued. The exception: when the
+ *   HIP runtime refuses one of the step's launches (REVISIT_ERR_LAUNCH), the
+ *   stages before it stay queued and the step does not advance; issuing
+ *   the same chunk again redoes them (each writes the same ring slot and
+ *   tables).
  * rc_stream_view -- device pointers to the last step's intermediate results
  *   (retrieval, layout tables, correspondence, packed cache) and its layout
  *   sizes, for inspection; valid until the next step or rc_stream_destroy.
@@ -430,17 +482,6 @@ int rc_stream_step(rc_stream* s, const float* depth, const float* c2w, const flo
                    hipStream_t stream);
 int rc_stream_view(const rc_stream* s, rc_stream_state* out);
 int rc_stream_destroy(rc_stream* s);
-
-/*
- * rc_set_attention_key_parts -- tuning knob of the bf16 attention work split
- * (not part of the method): the number of key parts P that later calls of
- * biased_chunk_attention cut each item into, process-wide (at most one part
- * per 32-key tile); 0 (the initial value) = chosen per call from the shape
- * and the compute units of the current device. Any value gives the same
- * results up to the fp32 rounding of the merge. Returns REVISIT_ERR_PARAM for
- * values outside [0, 64].
- */
-int rc_set_attention_key_parts(int32_t parts);
 
 #ifdef __cplusplus
 }

@@ -13,8 +13,11 @@ current HIP stream. The entry points mirror include/revisit.h:
 * ``biased_chunk_attention``   -- attention with the Gaussian correspondence
                                   bias (Sec. 4.3, Eq. bias)
 
-Each accepts optional preallocated outputs (``out=``) so a caller can run
-the path without allocating.
+Each accepts optional preallocated outputs (``out=``) and, where a kernel
+needs scratch memory, a preallocated ``workspace=`` (a uint8 GPU tensor of at
+least ``attention_workspace_size(...)`` / ``retrieve_workspace_size(...)``
+bytes), so a caller can run the path without allocating; without one the
+binding allocates the workspace with torch on the current stream.
 """
 
 from __future__ import annotations
@@ -28,7 +31,7 @@ from . import _lib
 from ._lib import BF16, F32, FP8_QK, MAX_K, RevisitError, last_error, lib, status_string  # noqa: F401
 
 __all__ = ["retrieve_chunks", "reproject_correspondence", "reproject_rotation", "biased_chunk_attention", "pack_retrieved_kv",
-           "pool_token_depth", "StreamDriver", "set_attention_key_parts",
+           "pool_token_depth", "StreamDriver", "attention_workspace_size", "retrieve_workspace_size",
            "RevisitError", "lib"]
 
 
@@ -56,9 +59,47 @@ def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape: Optional[Sequen
     return t
 
 
+def _workspace(nbytes: int, workspace: Optional[torch.Tensor], dev: torch.device, name: str):
+    """The caller's workspace (checked) or a fresh one of nbytes; None when nothing is needed."""
+    if workspace is not None:
+        _need(workspace, name, torch.uint8, None, dev)
+        return workspace
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=dev)
+
+
+def retrieve_workspace_size(n_bank: int, n_query: int, k: int) -> int:
+    """Bytes of workspace retrieve_chunks needs (0 for banks of at most 8192 entries)."""
+    n = ctypes.c_size_t(0)
+    _lib.check("rc_retrieve_workspace_size", lib().rc_retrieve_workspace_size(int(n_bank), int(n_query), int(k),
+                                                                              ctypes.byref(n)))
+    return int(n.value)
+
+
+def attention_workspace_size(dtype: torch.dtype, Lq: int, Lk: int, H: int, D: int, key_parts: int = 0) -> int:
+    """Bytes of workspace biased_chunk_attention needs on the current device
+    (dtype: torch.bfloat16, torch.float32 or torch.float8_e4m3fn for q)."""
+    n = ctypes.c_size_t(0)
+    _lib.check("rc_attention_workspace_size",
+               lib().rc_attention_workspace_size(_attn_dtype(dtype), int(Lq), int(Lk), int(H), int(D), int(key_parts),
+                                                 ctypes.byref(n)))
+    return int(n.value)
+
+
+def _attn_dtype(dtype: torch.dtype) -> int:
+    if dtype == torch.bfloat16:
+        return BF16
+    if dtype == torch.float32:
+        return F32
+    if dtype == torch.float8_e4m3fn:
+        return FP8_QK
+    raise TypeError(f"q must be bfloat16, float32 or float8_e4m3fn (got {dtype})")
+
+
 def retrieve_chunks(bank_c2w: torch.Tensor, query_c2w: torch.Tensor, query_chunk: torch.Tensor, *,
                     E: float, w_v: float, tau_c: float, tau_v: float, delta: int, first_candidate: int, k: int,
-                    frames_per_chunk: Optional[int] = None, out=None):
+                    frames_per_chunk: Optional[int] = None, out=None, workspace: Optional[torch.Tensor] = None):
     """Top-k pose retrieval. bank_c2w [N,4,4] f32, query_c2w [Q,4,4] f32,
     query_chunk [Q] i32. Returns (idx [Q,k] i32, score [Q,k] f32,
     count [Q] i32, frame_sel [Q,k*F] i32 or None)."""
@@ -82,9 +123,11 @@ def retrieve_chunks(bank_c2w: torch.Tensor, query_c2w: torch.Tensor, query_chunk
             raise ValueError("out frame_sel must be given exactly when frames_per_chunk is")
         if sel is not None:
             _need(sel, "out frame_sel", torch.int32, (Q, k * frames_per_chunk), dev)
+    ws = _workspace(retrieve_workspace_size(N, Q, k), workspace, dev, "workspace")
     st = lib().retrieve_chunks(_ptr(bank_c2w), N, _ptr(query_c2w), _ptr(query_chunk), Q, E, w_v, tau_c, tau_v,
                                delta, first_candidate, k, _ptr(idx), _ptr(score), _ptr(count),
-                               frames_per_chunk or 0, _ptr(sel), _stream(dev))
+                               frames_per_chunk or 0, _ptr(sel), _ptr(ws), ws.numel() if ws is not None else 0,
+                               _stream(dev))
     _lib.check("retrieve_chunks", st)
     return idx, score, count, sel
 
@@ -196,24 +239,19 @@ def reproject_rotation(tgt_c2w: torch.Tensor, tgt_K: torch.Tensor, src_c2w: torc
 def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv_frame_slot: torch.Tensor,
                            corr_uv: Optional[torch.Tensor], corr_idx: Optional[torch.Tensor], *,
                            h: int, w: int, softmax_scale: float, lam: float, sigma: float,
-                           return_lse: bool = True, out=None):
+                           return_lse: bool = True, out=None, key_parts: int = 0,
+                           workspace: Optional[torch.Tensor] = None):
     """Attention with the Gaussian correspondence bias on retrieved-frame keys.
 
     q [Lq,H,D], k, v [Lk,H,D] (bf16 with D=128, or fp32 with D in {64,128}, or
     q, k float8_e4m3fn with v bf16 and D=128: fp8 logits, o bf16);
     kv_frame_slot [Lk/(h*w)] i32; corr_uv [S,Lq,2] f32 and corr_idx [S,Lq] i32
-    (None = no bias). Returns (o [Lq,H,D], lse [H,Lq] f32 or None)."""
+    (None = no bias). key_parts: 0 = automatic key split, else a fixed
+    number of parts (1..64). Returns (o [Lq,H,D], lse [H,Lq] f32 or None)."""
     dev = q.device
     Lq, H, D = q.shape
     Lk = k.shape[0]
-    if q.dtype == torch.bfloat16:
-        dt = BF16
-    elif q.dtype == torch.float32:
-        dt = F32
-    elif q.dtype == torch.float8_e4m3fn:
-        dt = FP8_QK
-    else:
-        raise TypeError(f"q must be bfloat16, float32 or float8_e4m3fn (got {q.dtype})")
+    dt = _attn_dtype(q.dtype)
     vdt = torch.bfloat16 if dt == FP8_QK else q.dtype  # fp8 q, k come with bf16 v, o
     _need(q, "q", q.dtype, None, dev)
     _need(k, "k", q.dtype, (Lk, H, D), dev)
@@ -234,9 +272,13 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
         _need(o, "o", vdt, (Lq, H, D), dev)
         if lse is not None:
             _need(lse, "lse", torch.float32, (H, Lq), dev)
+    with torch.cuda.device(dev):
+        nbytes = attention_workspace_size(q.dtype, Lq, Lk, H, D, key_parts)
+    ws = _workspace(nbytes, workspace, dev, "workspace")
     st = lib().biased_chunk_attention(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), dt, Lq, Lk, H, D, h, w,
                                       _ptr(kv_frame_slot), _ptr(corr_uv), _ptr(corr_idx), S,
-                                      softmax_scale, lam, sigma, _stream(dev))
+                                      softmax_scale, lam, sigma, int(key_parts), _ptr(ws),
+                                      ws.numel() if ws is not None else 0, _stream(dev))
     _lib.check("biased_chunk_attention", st)
     return o, lse
 
@@ -361,10 +403,3 @@ class StreamDriver:
             self.close()
         except Exception:
             pass
-
-
-def set_attention_key_parts(parts: int) -> None:
-    """Key parts P that later bf16 attention calls cut each (head, query
-    tile) into, process-wide (0 = chosen per call). A tuning knob: results
-    agree up to the fp32 rounding of the partial-result merge for every P."""
-    _lib.check("rc_set_attention_key_parts", lib().rc_set_attention_key_parts(int(parts)))

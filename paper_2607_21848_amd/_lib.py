@@ -17,12 +17,14 @@ OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH, ERR_MEMORY = 0,
 BF16, F32, FP8_QK = 1, 2, 3
 MAX_K = 32
 EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
-            "reproject_rotation", "biased_chunk_attention", "rc_set_attention_key_parts", "pack_retrieved_kv", "pool_token_depth", "rc_stream_create",
-            "rc_stream_step", "rc_stream_view", "rc_stream_destroy")
+            "reproject_rotation", "biased_chunk_attention", "rc_retrieve_workspace_size", "rc_attention_workspace_size",
+            "pack_retrieved_kv", "pool_token_depth", "rc_stream_create", "rc_stream_step", "rc_stream_view",
+            "rc_stream_destroy")
 
 _p = ctypes.c_void_p
 _i = ctypes.c_int32
 _f = ctypes.c_float
+_z = ctypes.c_size_t
 
 
 class StreamConfig(ctypes.Structure):
@@ -60,7 +62,10 @@ def lib() -> ctypes.CDLL:
         L.rc_last_error.restype = ctypes.c_char_p
         L.rc_last_error.argtypes = []
         L.retrieve_chunks.restype = ctypes.c_int
-        L.retrieve_chunks.argtypes = [_p, _i, _p, _p, _i, _f, _f, _f, _f, _i, _i, _i, _p, _p, _p, _i, _p, _p]
+        L.retrieve_chunks.argtypes = [_p, _i, _p, _p, _i, _f, _f, _f, _f, _i, _i, _i, _p, _p, _p, _i, _p, _p, _z,
+                                      _p]
+        L.rc_retrieve_workspace_size.restype = ctypes.c_int
+        L.rc_retrieve_workspace_size.argtypes = [_i, _i, _i, ctypes.POINTER(ctypes.c_size_t)]
         L.reproject_correspondence.restype = ctypes.c_int
         L.reproject_correspondence.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _f,
                                                _p, _p, _p]
@@ -68,7 +73,9 @@ def lib() -> ctypes.CDLL:
         L.reproject_rotation.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p]
         L.biased_chunk_attention.restype = ctypes.c_int
         L.biased_chunk_attention.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _i,
-                                             _f, _f, _f, _p]
+                                             _f, _f, _f, _i, _p, _z, _p]
+        L.rc_attention_workspace_size.restype = ctypes.c_int
+        L.rc_attention_workspace_size.argtypes = [_i, _i, _i, _i, _i, _i, ctypes.POINTER(ctypes.c_size_t)]
         L.pack_retrieved_kv.restype = ctypes.c_int
         L.pack_retrieved_kv.argtypes = [_p, _p, _p, _i, _p, _i, _i, _p, _p, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i,
                                         _f, _p]
@@ -82,8 +89,6 @@ def lib() -> ctypes.CDLL:
         L.rc_stream_view.argtypes = [_p, ctypes.POINTER(StreamState)]
         L.rc_stream_destroy.restype = ctypes.c_int
         L.rc_stream_destroy.argtypes = [_p]
-        L.rc_set_attention_key_parts.restype = ctypes.c_int
-        L.rc_set_attention_key_parts.argtypes = [_i]
         _LIB = L
     return _LIB
 

@@ -15,7 +15,7 @@ import sys
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG_DIR, "csrc")
 LIB_PATH = os.path.join(PKG_DIR, "librevisit.so")
-SOURCES = ["capi.cpp", "workspace.cpp", "retrieve.hip", "reproject.hip", "attention.hip", "kvpack.hip", "stream.cpp", "stream_kernels.hip"]
+SOURCES = ["capi.cpp", "retrieve.hip", "reproject.hip", "attention.hip", "kvpack.hip", "stream.cpp", "stream_kernels.hip"]
 ARCH = "gfx950"
 
 

@@ -1,14 +1,13 @@
 // C entry points of librevisit: argument validation on the host, then the
-// kernel launches on the caller's stream. State: a per-thread last-error
-// string, the bf16 attention key-part setting, and the attention workspace
-// (workspace.cpp). The streaming driver's entry points are in stream.cpp.
+// kernel launches on the caller's stream. The only state is a per-thread
+// last-error string; scratch memory comes from the caller (workspace
+// arguments sized by the rc_*_workspace_size queries). The streaming driver's
+// entry points are in stream.cpp.
 
 #include <math.h>
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
-
-#include <atomic>
 
 #include <hip/hip_runtime.h>
 
@@ -40,9 +39,65 @@ constexpr int64_t kMaxElems = (int64_t)1 << 40;
 constexpr int kMaxFrames = 1024;
 constexpr int kMaxGridSide = 256;  // token-grid rows / columns of the bf16 kernel's bias tables
 constexpr int kMaxKeyParts = 64;
+constexpr uintptr_t kWorkspaceAlign = 16;
 
-// key parts of the bf16 attention kernel; 0 = chosen per call
-std::atomic<int> g_attention_key_parts{0};
+// Checks a caller's workspace against the bytes a call needs.
+int check_workspace(const char* fn, size_t need, const void* ws, size_t ws_bytes) {
+    if (need == 0) return REVISIT_OK;
+    if (ws_bytes < need)
+        return fail(REVISIT_ERR_SHAPE, "%s: workspace of %zu bytes given, %zu needed", fn, ws_bytes, need);
+    if (!ws) return fail(REVISIT_ERR_NULL, "%s: workspace is NULL (%zu bytes needed)", fn, need);
+    if (!aligned(ws, kWorkspaceAlign)) return fail(REVISIT_ERR_SHAPE, "%s: workspace must be 16-byte aligned", fn);
+    return REVISIT_OK;
+}
+
+// Compute units of the current device.
+hipError_t device_compute_units(int* cus) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    return hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
+}
+
+// Shape, dtype and key-part checks shared by biased_chunk_attention and
+// rc_attention_workspace_size.
+int check_attention_shape(const char* fn, int32_t dtype, int32_t Lq, int32_t Lk, int32_t H, int32_t D,
+                          int32_t key_parts) {
+    if (dtype != REVISIT_BF16 && dtype != REVISIT_F32 && dtype != REVISIT_FP8_QK)
+        return fail(REVISIT_ERR_UNSUPPORTED, "%s: dtype %d not supported", fn, dtype);
+    if ((dtype == REVISIT_BF16 || dtype == REVISIT_FP8_QK) && D != 128)
+        return fail(REVISIT_ERR_UNSUPPORTED, "%s: bf16 / fp8 needs D = 128 (got %d)", fn, D);
+    if (dtype == REVISIT_F32 && D != 64 && D != 128)
+        return fail(REVISIT_ERR_UNSUPPORTED, "%s: fp32 needs D = 64 or 128 (got %d)", fn, D);
+    if (Lq < 0 || Lk < 1 || H < 1) return fail(REVISIT_ERR_SHAPE, "%s: need Lq >= 0, Lk >= 1, H >= 1", fn);
+    if (H > 65535) return fail(REVISIT_ERR_SHAPE, "%s: H > 65535", fn);
+    if ((int64_t)Lk * H * D > kMaxElems || (int64_t)Lq * H * D > kMaxElems)
+        return fail(REVISIT_ERR_SHAPE, "%s: problem too large", fn);
+    // (head, key part, 128-query tile) workgroups of the bf16 kernel: a 32-bit count
+    if (((int64_t)Lq + 127) / 128 * H * kMaxKeyParts > ((int64_t)1 << 31))
+        return fail(REVISIT_ERR_SHAPE, "%s: problem too large", fn);
+    if (key_parts < 0 || key_parts > kMaxKeyParts)
+        return fail(REVISIT_ERR_PARAM, "%s: key_parts=%d outside [0, %d]", fn, key_parts, kMaxKeyParts);
+    return REVISIT_OK;
+}
+
+// Key parts of the bf16 / fp8 kernel for this call (0 = automatic), and the
+// workspace bytes they need. AttentionArgs needs only Lq, Lk and H here.
+int attention_parts(const char* fn, const revisit::AttentionArgs& a, int32_t key_parts, int32_t* parts,
+                    size_t* bytes) {
+    int32_t P = key_parts;
+    if (P == 0) {
+        int cus = 0;
+        const hipError_t e = device_compute_units(&cus);
+        if (e != hipSuccess) return fail(REVISIT_ERR_LAUNCH, "%s: device query failed: %s", fn, hipGetErrorString(e));
+        P = revisit::attention_bf16_key_parts(a, 2 * cus);  // two resident workgroups per compute unit
+    }
+    const int32_t tiles = (a.Lk + 31) / 32;
+    P = P < tiles ? P : tiles;  // at least one key tile per part
+    *parts = P;
+    *bytes = revisit::attention_bf16_workspace_bytes(a, P);
+    return REVISIT_OK;
+}
 
 }  // namespace
 
@@ -76,10 +131,11 @@ const char* rc_last_error(void) { return g_last_error; }
 int retrieve_chunks(const float* bank_c2w, int32_t n_bank, const float* query_c2w, const int32_t* query_chunk,
                     int32_t n_query, float E, float w_v, float tau_c, float tau_v, int32_t delta,
                     int32_t first_candidate, int32_t k, int32_t* out_idx, float* out_score, int32_t* out_count,
-                    int32_t frames_per_chunk, int32_t* out_frame_sel, hipStream_t stream) {
-    if (n_bank < 0 || n_query < 0) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: negative n_bank or n_query");
-    if (n_bank > (1 << 30)) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: n_bank=%d above 2^30", n_bank);
-    if (k < 1 || k > REVISIT_MAX_K) return fail(REVISIT_ERR_PARAM, "retrieve_chunks: k=%d outside [1, %d]", k, REVISIT_MAX_K);
+                    int32_t frames_per_chunk, int32_t* out_frame_sel, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+    size_t need = 0;
+    int st = rc_retrieve_workspace_size(n_bank, n_query, k, &need);
+    if (st != REVISIT_OK) return st;
     if (!(finite(E) && E > 0.0f)) return fail(REVISIT_ERR_PARAM, "retrieve_chunks: E must be finite and > 0");
     if (!finite(w_v) || !finite(tau_c) || !finite(tau_v))
         return fail(REVISIT_ERR_PARAM, "retrieve_chunks: w_v, tau_c and tau_v must be finite");
@@ -111,18 +167,26 @@ int retrieve_chunks(const float* bank_c2w, int32_t n_bank, const float* query_c2
     a.n_seg = revisit::retrieve_segments(n_bank);
     a.seg_s = nullptr;
     a.seg_j = nullptr;
+    st = check_workspace("retrieve_chunks", need, workspace, workspace_bytes);
+    if (st != REVISIT_OK) return st;
     if (a.n_seg > 0) {
-        if ((int64_t)a.n_seg * n_query * k > ((int64_t)1 << 31))
-            return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: n_bank * n_query too large");
-        void* ws = nullptr;
-        const hipError_t e = revisit::stream_workspace(stream, revisit::retrieve_workspace_bytes(n_bank, n_query, k), &ws);
-        if (e != hipSuccess)
-            return fail(e == hipErrorOutOfMemory ? REVISIT_ERR_MEMORY : REVISIT_ERR_LAUNCH, "retrieve_chunks: workspace: %s",
-                        hipGetErrorString(e));
-        a.seg_s = static_cast<double*>(ws);
+        a.seg_s = static_cast<double*>(workspace);
         a.seg_j = reinterpret_cast<int32_t*>(a.seg_s + (size_t)a.n_seg * n_query * k);
     }
     return launched(revisit::launch_retrieve(a, stream), "retrieve_chunks");
+}
+
+int rc_retrieve_workspace_size(int32_t n_bank, int32_t n_query, int32_t k, size_t* bytes) {
+    if (!bytes) return fail(REVISIT_ERR_NULL, "rc_retrieve_workspace_size: bytes is NULL");
+    *bytes = 0;
+    if (n_bank < 0 || n_query < 0) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: negative n_bank or n_query");
+    if (n_bank > (1 << 30)) return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: n_bank=%d above 2^30", n_bank);
+    if (k < 1 || k > REVISIT_MAX_K) return fail(REVISIT_ERR_PARAM, "retrieve_chunks: k=%d outside [1, %d]", k, REVISIT_MAX_K);
+    const int32_t n_seg = revisit::retrieve_segments(n_bank);
+    if (n_seg > 0 && (int64_t)n_seg * n_query * k > ((int64_t)1 << 31))
+        return fail(REVISIT_ERR_SHAPE, "retrieve_chunks: n_bank * n_query too large");
+    *bytes = n_seg > 0 ? revisit::retrieve_workspace_bytes(n_bank, n_query, k) : 0;
+    return REVISIT_OK;
 }
 
 int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const float* tgt_K,
@@ -164,6 +228,7 @@ int reproject_correspondence(const float* tgt_depth, const float* tgt_c2w, const
     a.eps = (double)eps;
     a.out_uv = out_uv;
     a.out_idx = out_idx;
+    a.paired = 0;
     return launched(revisit::launch_reproject(a, stream), "reproject_correspondence");
 }
 
@@ -203,30 +268,22 @@ int reproject_rotation(const float* tgt_c2w, const float* tgt_K, const float* sr
     a.eps = 0.0;
     a.out_uv = out_uv;
     a.out_idx = out_idx;
+    a.paired = aligned(out_uv, 16) && aligned(out_idx, 8);
     return launched(revisit::launch_rotation(a, stream), "reproject_rotation");
 }
 
 int biased_chunk_attention(const void* q, const void* k, const void* v, void* o, float* lse, int32_t dtype,
                            int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
                            const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx, int32_t S,
-                           float softmax_scale, float lambda, float sigma, hipStream_t stream) {
-    if (dtype != REVISIT_BF16 && dtype != REVISIT_F32 && dtype != REVISIT_FP8_QK)
-        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: dtype %d not supported", dtype);
-    if ((dtype == REVISIT_BF16 || dtype == REVISIT_FP8_QK) && D != 128)
-        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: bf16 / fp8 needs D = 128 (got %d)", D);
-    if (dtype == REVISIT_F32 && D != 64 && D != 128)
-        return fail(REVISIT_ERR_UNSUPPORTED, "biased_chunk_attention: fp32 needs D = 64 or 128 (got %d)", D);
-    if (Lq < 0 || Lk < 1 || H < 1 || h < 1 || w < 1 || S < 0)
-        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: need Lq >= 0, Lk >= 1, H, h, w >= 1, S >= 0");
-    if (H > 65535) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: H > 65535");
+                           float softmax_scale, float lambda, float sigma, int32_t key_parts, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+    int st = check_attention_shape("biased_chunk_attention", dtype, Lq, Lk, H, D, key_parts);
+    if (st != REVISIT_OK) return st;
+    if (h < 1 || w < 1 || S < 0) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: need h, w >= 1, S >= 0");
     const int64_t hw = (int64_t)h * w;
     if (Lk % hw != 0) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: Lk=%d not a multiple of h*w=%lld", Lk, (long long)hw);
     if (Lk / hw > kMaxFrames) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: more than %d KV frames", kMaxFrames);
-    if ((int64_t)Lk * H * D > kMaxElems || (int64_t)Lq * H * D > kMaxElems || (int64_t)S * Lq > kMaxElems)
-        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: problem too large");
-    // (head, key part, 128-query tile) workgroups of the bf16 kernel: a 32-bit count
-    if (((int64_t)Lq + 127) / 128 * H * kMaxKeyParts > ((int64_t)1 << 31))
-        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: problem too large");
+    if ((int64_t)S * Lq > kMaxElems) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: problem too large");
     if (!(finite(softmax_scale) && softmax_scale > 0.0f))
         return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: softmax_scale must be finite and > 0");
     if (!(finite(sigma) && sigma > 0.0f)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: sigma must be finite and > 0");
@@ -267,21 +324,28 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     a.sigma = sigma;
     a.fp8_qk = dtype == REVISIT_FP8_QK;
     if (dtype == REVISIT_F32) return launched(revisit::launch_attention_f32(a, stream), "biased_chunk_attention");
-    if (Lq == 0) return REVISIT_OK;
-    int32_t parts = g_attention_key_parts.load();
-    if (parts == 0) {
-        int cus = 0;
-        const hipError_t e = revisit::device_compute_units(&cus);
-        if (e != hipSuccess) return launched(e, "biased_chunk_attention");
-        parts = revisit::attention_bf16_key_parts(a, 2 * cus);  // two resident workgroups per compute unit
-    }
-    parts = parts < (Lk + 31) / 32 ? parts : (Lk + 31) / 32;  // at least one key tile per part
-    void* ws = nullptr;
-    const hipError_t e = revisit::stream_workspace(stream, revisit::attention_bf16_workspace_bytes(a, parts), &ws);
-    if (e != hipSuccess)
-        return fail(e == hipErrorOutOfMemory ? REVISIT_ERR_MEMORY : REVISIT_ERR_LAUNCH,
-                    "biased_chunk_attention: workspace: %s", hipGetErrorString(e));
-    return launched(revisit::launch_attention_bf16(a, parts, static_cast<float*>(ws), stream), "biased_chunk_attention");
+    int32_t parts = 1;
+    size_t need = 0;
+    st = attention_parts("biased_chunk_attention", a, key_parts, &parts, &need);
+    if (st != REVISIT_OK) return st;
+    st = check_workspace("biased_chunk_attention", need, workspace, workspace_bytes);
+    if (st != REVISIT_OK) return st;
+    return launched(revisit::launch_attention_bf16(a, parts, static_cast<float*>(workspace), stream),
+                    "biased_chunk_attention");
+}
+
+int rc_attention_workspace_size(int32_t dtype, int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t key_parts,
+                                size_t* bytes) {
+    if (!bytes) return fail(REVISIT_ERR_NULL, "rc_attention_workspace_size: bytes is NULL");
+    *bytes = 0;
+    const int st = check_attention_shape("rc_attention_workspace_size", dtype, Lq, Lk, H, D, key_parts);
+    if (st != REVISIT_OK || dtype == REVISIT_F32 || Lq == 0) return st;
+    revisit::AttentionArgs a{};
+    a.Lq = Lq;
+    a.Lk = Lk;
+    a.H = H;
+    int32_t parts = 1;
+    return attention_parts("rc_attention_workspace_size", a, key_parts, &parts, bytes);
 }
 
 int pack_retrieved_kv(const void* store_k, const void* store_v, const int32_t* store_pos, int32_t n_store,
@@ -349,13 +413,6 @@ int pool_token_depth(const float* depth, int32_t n_frames, int32_t h, int32_t w,
     if (!depth || !out) return fail(REVISIT_ERR_NULL, "pool_token_depth: depth and out are required");
     if (!aligned(depth, 4) || !aligned(out, 4)) return fail(REVISIT_ERR_SHAPE, "pool_token_depth: arrays must be 4-byte aligned");
     return launched(revisit::launch_pool_depth(depth, (int64_t)n_frames * h * w, h, w, p, out, stream), "pool_token_depth");
-}
-
-int rc_set_attention_key_parts(int32_t parts) {
-    if (parts < 0 || parts > kMaxKeyParts)
-        return fail(REVISIT_ERR_PARAM, "rc_set_attention_key_parts: %d outside [0, %d]", parts, kMaxKeyParts);
-    g_attention_key_parts.store(parts);
-    return REVISIT_OK;
 }
 
 }  // extern "C"

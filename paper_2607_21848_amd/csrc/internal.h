@@ -58,6 +58,9 @@ struct ReprojectArgs {
     double eps;
     float* out_uv;
     int32_t* out_idx;
+    // rotation path: out_uv is 16-byte and out_idx 8-byte aligned, so an
+    // even token index starts an aligned pair of both
+    int32_t paired;
 };
 hipError_t launch_reproject(const ReprojectArgs& a, hipStream_t stream);
 // rotation-only correspondence: ReprojectArgs with the depth maps and eps unused
@@ -147,11 +150,6 @@ struct StreamSlotsArgs {
 hipError_t launch_stream_slots(const StreamSlotsArgs& a, hipStream_t stream);
 hipError_t launch_pool_depth(const float* depth, int64_t n_tokens, int32_t h, int32_t w, int32_t p, float* out,
                              hipStream_t stream);
-
-// Library-owned device memory of `bytes` for work queued on `stream` of the
-// current device (see workspace.cpp); compute units of the current device.
-hipError_t stream_workspace(hipStream_t stream, size_t bytes, void** out);
-hipError_t device_compute_units(int* cus);
 
 // Sets the calling thread's last-error string and returns status (capi.cpp).
 int fail_status(int status, const char* fmt, ...);

@@ -57,6 +57,8 @@ struct rc_stream {
     int32_t* src_sel;
     int32_t* store_pos;
     int32_t* zero;
+    void* workspace;  // attention key split and retrieval scratch of the largest step
+    size_t workspace_bytes;
     // the last step's layout
     int32_t last_n, last_parts, last_ret_part;
 };
@@ -89,7 +91,7 @@ void release(rc_stream* s) {
     void* bufs[] = {s->bank,      s->ring_depth, s->ring_c2w,   s->ring_K,      s->ring_k,    s->ring_v,
                     s->cache_k,   s->cache_v,    s->corr_uv,    s->corr_idx,    s->ret_idx,   s->ret_score,
                     s->ret_count, s->query_chunk, s->part_slot, s->kv_slot,     s->src_sel,   s->store_pos,
-                    s->zero};
+                    s->zero,      s->workspace};
     for (void* b : bufs)
         if (b) (void)hipFree(b);
 }
@@ -103,6 +105,8 @@ bool alloc(Ptr** p, size_t bytes) {
 }
 
 bool is_finite(float x) { return isfinite(x); }
+
+bool aligned(const void* ptr, uintptr_t bytes) { return ((uintptr_t)ptr % bytes) == 0; }
 
 }  // namespace
 
@@ -157,6 +161,28 @@ int rc_stream_create(const rc_stream_config* cfg, rc_stream** out) {
         delete s;
         return revisit::fail_status(REVISIT_ERR_LAUNCH, "rc_stream_create: no current device");
     }
+    // workspace of the largest step on this device: attention over 1..5 parts of
+    // T keys (the automatic key split), retrieval over up to max_chunks entries
+    size_t ws = 0;
+    for (int32_t np = 1; np <= revisit::kStreamMaxParts; ++np) {
+        size_t b = 0;
+        const int st = rc_attention_workspace_size(c.dtype, (int32_t)T, np * (int32_t)T, c.H, c.D, 0, &b);
+        if (st != REVISIT_OK) {
+            delete s;
+            return st;
+        }
+        ws = b > ws ? b : ws;
+    }
+    {
+        size_t b = 0;
+        const int st = rc_retrieve_workspace_size(c.max_chunks, 1, 1, &b);
+        if (st != REVISIT_OK) {
+            delete s;
+            return st;
+        }
+        ws = b > ws ? b : ws;
+    }
+    s->workspace_bytes = ws;
     const size_t C = (size_t)c.capacity, F = (size_t)c.F, hw = (size_t)c.h * c.w;
     const size_t kv_ring = (size_t)c.layers * C * T * c.H * c.D * s->esize;
     const size_t kv_cache = (size_t)c.layers * s->max_rows * c.H * c.D * s->esize;
@@ -168,7 +194,7 @@ int rc_stream_create(const rc_stream_config* cfg, rc_stream** out) {
                     alloc(&s->ret_count, 16) && alloc(&s->query_chunk, 16) &&
                     alloc(&s->part_slot, revisit::kStreamMaxParts * 4) &&
                     alloc(&s->kv_slot, revisit::kStreamMaxParts * F * 4) && alloc(&s->src_sel, F * 4) &&
-                    alloc(&s->store_pos, C * 4) && alloc(&s->zero, 16);
+                    alloc(&s->store_pos, C * 4) && alloc(&s->zero, 16) && alloc(&s->workspace, ws);
     if (!ok) {
         release(s);
         delete s;
@@ -217,6 +243,12 @@ int rc_stream_step(rc_stream* s, const float* depth, const float* c2w, const flo
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess || cur != s->device)
         return revisit::fail_status(REVISIT_ERR_PARAM, "rc_stream_step: the stream's device is not current");
+    // the configuration was validated at creation; with these alignments every
+    // stage call below passes its own validation, so only a launch can fail
+    if (!aligned(depth, 4) || !aligned(c2w, 4) || !aligned(K, 4) || !aligned(q, 16) || !aligned(k, 16) ||
+        !aligned(v, 16) || !aligned(o, 16) || !aligned(lse, 4))
+        return revisit::fail_status(REVISIT_ERR_SHAPE, "rc_stream_step: q, k, v, o must be 16-byte aligned, "
+                                                       "depth, c2w, K and lse 4-byte");
     const int32_t n = s->n, F = c.F, T = s->T, C = c.capacity, hw = c.h * c.w;
     const size_t row = (size_t)c.H * c.D * s->esize;
     const int32_t slot_n = ring_slot(n, C);
@@ -235,7 +267,8 @@ int rc_stream_step(rc_stream* s, const float* depth, const float* c2w, const flo
     if (n >= 1) {
         const int32_t first = n - C + 2 > 1 ? n - C + 2 : 1;
         st = retrieve_chunks(s->bank, n, s->bank + (size_t)n * 16, s->query_chunk, 1, c.E, c.w_v, c.tau_c, c.tau_v,
-                             c.delta, first, 1, s->ret_idx, s->ret_score, s->ret_count, 0, nullptr, stream);
+                             c.delta, first, 1, s->ret_idx, s->ret_score, s->ret_count, 0, nullptr, s->workspace,
+                             s->workspace_bytes, stream);
         if (st != REVISIT_OK) return st;
     }
 
@@ -287,7 +320,7 @@ int rc_stream_step(rc_stream* s, const float* depth, const float* c2w, const flo
                                     static_cast<const uint8_t*>(s->cache_v) + co, static_cast<uint8_t*>(o) + qo,
                                     lse ? lse + (size_t)l * c.H * T : nullptr, c.dtype, T, Lk, c.H, c.D, c.h, c.w,
                                     s->kv_slot, s->corr_uv, s->corr_idx, ret_part >= 0 ? F : 0, c.softmax_scale,
-                                    c.lambda, c.sigma, stream);
+                                    c.lambda, c.sigma, 0, s->workspace, s->workspace_bytes, stream);
         if (st != REVISIT_OK) return st;
     }
     s->last_n = n;

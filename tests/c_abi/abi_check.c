@@ -43,9 +43,33 @@ static void host_checks(void) {
     CHECK(strlen(rc_status_string(REVISIT_ERR_NULL)) > 0, "status string of REVISIT_ERR_NULL");
 
     int st = retrieve_chunks(NULL, 10, FAKE, FAKE, 1, 1.0f, 0.5f, 0.1f, 0.5f, 3, 1, 4, FAKE, NULL, FAKE, 0, NULL,
-                             NULL);
+                             NULL, 0, NULL);
     CHECK(st == REVISIT_ERR_NULL, "retrieve_chunks with a NULL bank: %d", st);
     CHECK(strlen(rc_last_error()) > 0, "rc_last_error after a failure");
+
+    /* workspace sizes: 2 queries x 64 segments of 16384 entries x k = 4 x 12 bytes */
+    size_t bytes = 1;
+    st = rc_retrieve_workspace_size(1 << 20, 2, 4, &bytes);
+    CHECK(st == REVISIT_OK && bytes == (size_t)2 * 64 * 4 * 12, "retrieval workspace of a 2^20 bank: %d, %zu", st,
+          bytes);
+    st = rc_retrieve_workspace_size(8192, 2, 4, &bytes);
+    CHECK(st == REVISIT_OK && bytes == 0, "retrieval workspace of an 8192-entry bank: %d, %zu", st, bytes);
+    st = retrieve_chunks(FAKE, 1 << 20, FAKE, FAKE, 2, 1.0f, 0.5f, 0.1f, 0.5f, 3, 1, 4, FAKE, NULL, FAKE, 0, NULL,
+                         NULL, 0, NULL);
+    CHECK(st == REVISIT_ERR_SHAPE, "retrieve_chunks over a 2^20 bank without a workspace: %d", st);
+    /* 37 query tiles x 12 heads = 444 items, 4 parts of 128 x 128 + 2 x 128 floats */
+    st = rc_attention_workspace_size(REVISIT_BF16, 4680, 37440, 12, 128, 4, &bytes);
+    CHECK(st == REVISIT_OK && bytes == (size_t)444 * 4 * 16640 * 4, "attention workspace in 4 parts: %d, %zu", st,
+          bytes);
+    st = rc_attention_workspace_size(REVISIT_BF16, 4680, 37440, 12, 128, 1, &bytes);
+    CHECK(st == REVISIT_OK && bytes == 0, "attention workspace in 1 part: %d, %zu", st, bytes);
+    st = rc_attention_workspace_size(REVISIT_F32, 4680, 37440, 12, 128, 4, &bytes);
+    CHECK(st == REVISIT_OK && bytes == 0, "fp32 attention workspace: %d, %zu", st, bytes);
+    st = rc_attention_workspace_size(REVISIT_BF16, 4680, 37440, 12, 128, 65, &bytes);
+    CHECK(st == REVISIT_ERR_PARAM, "attention workspace with 65 key parts: %d", st);
+    st = biased_chunk_attention(FAKE, FAKE, FAKE, FAKE, NULL, REVISIT_BF16, 4680, 37440, 12, 128, 30, 52, FAKE, FAKE,
+                                FAKE, 12, 0.088f, 1.0f, 2.0f, 4, FAKE, 4096, NULL);
+    CHECK(st == REVISIT_ERR_SHAPE, "biased_chunk_attention with a 4 KiB workspace for 4 key parts: %d", st);
 
     st = reproject_correspondence(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NULL, 0, 1, 3, 6, 30, 52, 2, -1.0f, FAKE, FAKE,
                                   NULL);
@@ -57,7 +81,7 @@ static void host_checks(void) {
     CHECK(st == REVISIT_ERR_SHAPE, "reproject_rotation with 65 sources: %d", st);
 
     st = biased_chunk_attention(FAKE, FAKE, FAKE, FAKE, NULL, REVISIT_BF16, 4680, 28080, 12, 128, 30, 52, FAKE, FAKE,
-                                FAKE, 6, 0.088f, 1.0f, 0.0f, NULL);
+                                FAKE, 6, 0.088f, 1.0f, 0.0f, 0, NULL, 0, NULL);
     CHECK(st == REVISIT_ERR_PARAM, "biased_chunk_attention with sigma = 0: %d", st);
 
     st = pack_retrieved_kv(FAKE, FAKE, NULL, 200, FAKE, 4, 3, NULL, FAKE, 4680, 37440, 30, REVISIT_BF16, 3, 30, 52, 12,
@@ -70,9 +94,6 @@ static void host_checks(void) {
     rc_stream* s = NULL;
     st = rc_stream_create(NULL, &s);
     CHECK(st == REVISIT_ERR_NULL && s == NULL, "rc_stream_create without a configuration: %d", st);
-
-    CHECK(rc_set_attention_key_parts(-1) == REVISIT_ERR_PARAM, "rc_set_attention_key_parts(-1)");
-    CHECK(rc_set_attention_key_parts(0) == REVISIT_OK, "rc_set_attention_key_parts(0)");
 }
 
 /* one problem: Tq = 1 target frame, S = 2 sources, an h x w grid at p = 2 */

@@ -31,7 +31,7 @@ def test_header_declares_the_three_stages():
     names = declared_functions()
     for n in ("retrieve_chunks", "reproject_correspondence", "reproject_rotation", "biased_chunk_attention",
               "pack_retrieved_kv",
-              "rc_status_string", "rc_last_error", "rc_set_attention_key_parts"):
+              "rc_status_string", "rc_last_error", "rc_retrieve_workspace_size", "rc_attention_workspace_size"):
         assert n in names
 
 
@@ -58,11 +58,11 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
 
 def _retrieve(L, **kw):
     a = dict(bank=FAKE, n_bank=10, query=FAKE, qchunk=FAKE, n_query=1, E=1.0, w_v=0.5, tau_c=0.1, tau_v=0.5,
-             delta=3, first=1, k=4, idx=FAKE, score=NULL, count=FAKE, F=0, sel=NULL)
+             delta=3, first=1, k=4, idx=FAKE, score=NULL, count=FAKE, F=0, sel=NULL, ws=NULL, ws_bytes=0)
     a.update(kw)
     return L.retrieve_chunks(a["bank"], a["n_bank"], a["query"], a["qchunk"], a["n_query"], a["E"], a["w_v"],
                              a["tau_c"], a["tau_v"], a["delta"], a["first"], a["k"], a["idx"], a["score"],
-                             a["count"], a["F"], a["sel"], NULL)
+                             a["count"], a["F"], a["sel"], a["ws"], a["ws_bytes"], NULL)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -70,6 +70,9 @@ def _retrieve(L, **kw):
     (dict(n_bank=-1), 2), (dict(n_bank=(1 << 30) + 1), 2), (dict(n_query=-2), 2), (dict(query=NULL), 1),
     (dict(count=NULL), 1), (dict(bank=ctypes.c_void_p(0x1004)), 2),
     (dict(sel=FAKE, F=0), 4),
+    # a bank above 8192 entries needs a workspace: none, too small, NULL, misaligned
+    (dict(n_bank=20000), 2), (dict(n_bank=20000, ws=FAKE, ws_bytes=95), 2), (dict(n_bank=20000, ws_bytes=96), 1),
+    (dict(n_bank=20000, ws=ctypes.c_void_p(0x1008), ws_bytes=96), 2),
 ])
 def test_retrieve_rejects(L, kw, status):
     from paper_2607_21848_amd import _lib
@@ -133,11 +136,12 @@ def test_rotation_empty_is_ok(L):
 
 def _attention(L, **kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=NULL, dtype=1, Lq=4680, Lk=28080, H=12, D=128, h=30, w=52,
-             slot=FAKE, uv=FAKE, idx=FAKE, S=6, scale=1 / math.sqrt(128), lam=1.0, sigma=2.0)
+             slot=FAKE, uv=FAKE, idx=FAKE, S=6, scale=1 / math.sqrt(128), lam=1.0, sigma=2.0, parts=3, ws=NULL,
+             ws_bytes=0)
     a.update(kw)
     return L.biased_chunk_attention(a["q"], a["k"], a["v"], a["o"], a["lse"], a["dtype"], a["Lq"], a["Lk"], a["H"],
                                     a["D"], a["h"], a["w"], a["slot"], a["uv"], a["idx"], a["S"], a["scale"],
-                                    a["lam"], a["sigma"], NULL)
+                                    a["lam"], a["sigma"], a["parts"], a["ws"], a["ws_bytes"], NULL)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -145,6 +149,10 @@ def _attention(L, **kw):
     (dict(H=0), 2), (dict(Lq=-1), 2), (dict(sigma=0.0), 4), (dict(scale=-1.0), 4), (dict(lam=float("inf")), 4),
     (dict(sigma=1e-30), 4), (dict(q=NULL), 1), (dict(o=NULL), 1), (dict(uv=NULL), 1), (dict(slot=NULL), 1),
     (dict(Lk=1025 * 1560), 2), (dict(h=300, w=4, Lk=1200 * 8), 2), (dict(dtype=3, h=4, w=257, Lk=1028 * 8), 2),
+    (dict(parts=-1), 4), (dict(parts=65), 4),
+    # 3 key parts of 444 items need 444 * 3 * 66560 bytes: none, one byte short, NULL, misaligned
+    (dict(), 2), (dict(ws=FAKE, ws_bytes=444 * 3 * 66560 - 1), 2), (dict(ws_bytes=444 * 3 * 66560), 1),
+    (dict(ws=ctypes.c_void_p(0x1004), ws_bytes=444 * 3 * 66560), 2),
 ])
 def test_attention_rejects(L, kw, status):
     assert _attention(L, **kw) == status
@@ -156,10 +164,36 @@ def test_attention_bias_pointers_optional_when_off(L):
     assert _attention(L, Lq=0, lam=0.0, uv=NULL, idx=NULL, slot=NULL) == 0
 
 
-@pytest.mark.parametrize("n,status", [(-1, 4), (65, 4), (7, 0), (64, 0), (0, 0)])
-def test_attention_key_parts_knob(L, n, status):
-    assert L.rc_set_attention_key_parts(n) == status
-    L.rc_set_attention_key_parts(0)
+def _ws_size(L, fn, *args):
+    n = ctypes.c_size_t(12345)
+    st = getattr(L, fn)(*args, ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("args,status,nbytes", [
+    ((1, 4680, 37440, 12, 128, 4), 0, 444 * 4 * 66560), ((1, 4680, 37440, 12, 128, 1), 0, 0),
+    ((3, 4680, 37440, 12, 128, 2), 0, 444 * 2 * 66560), ((2, 4680, 37440, 12, 128, 8), 0, 0),
+    ((1, 0, 37440, 12, 128, 8), 0, 0), ((1, 4680, 64, 12, 128, 8), 0, 444 * 2 * 66560),
+    ((1, 4680, 37440, 12, 128, -1), 4, 0), ((1, 4680, 37440, 12, 128, 65), 4, 0), ((1, 4680, 37440, 12, 64, 4), 3, 0),
+    ((9, 4680, 37440, 12, 128, 4), 3, 0), ((1, -1, 37440, 12, 128, 4), 2, 0), ((1, 4680, 0, 12, 128, 4), 2, 0),
+])
+def test_attention_workspace_size(L, args, status, nbytes):
+    """Fixed key parts need no device: items * parts * (128 x 128 + 2 x 128) floats,
+    nothing for one part or fp32, parts clamped to the number of 32-key tiles."""
+    assert _ws_size(L, "rc_attention_workspace_size", *args) == (status, nbytes)
+
+
+@pytest.mark.parametrize("args,status,nbytes", [
+    ((8192, 5, 4), 0, 0), ((8193, 5, 4), 0, 5 * 1 * 4 * 12), ((1 << 23, 1, 32), 0, 512 * 32 * 12),
+    ((0, 1, 1), 0, 0), ((-1, 1, 1), 2, 0), ((10, 1, 0), 4, 0), ((10, 1, 33), 4, 0), ((1 << 30, 1 << 20, 32), 2, 0),
+])
+def test_retrieve_workspace_size(L, args, status, nbytes):
+    assert _ws_size(L, "rc_retrieve_workspace_size", *args) == (status, nbytes)
+
+
+def test_workspace_size_null_out(L):
+    assert L.rc_attention_workspace_size(1, 10, 10, 1, 128, 1, None) == 1
+    assert L.rc_retrieve_workspace_size(10, 1, 1, None) == 1
 
 
 def _pack(L, **kw):

@@ -1,9 +1,9 @@
 """Concurrent use of the library: two host threads, each with its own HIP
-stream, run bf16 attention with the key split (which takes the per-stream
-workspace) and a segmented retrieval (the same workspace) at the same time,
+stream and its own workspace, run bf16 attention with the key split (its
+partial results in the workspace) and a segmented retrieval (candidates in
+the same workspace, after the attention on that stream) at the same time,
 several rounds each. Every result must equal the one computed alone: the
-workspace blocks of different streams never alias, and the registry and the
-per-thread error string are safe under concurrent calls."""
+library keeps no state that two streams could share."""
 
 from __future__ import annotations
 
@@ -44,37 +44,39 @@ def test_two_threads_two_streams():
     cases = [(_attention_case(s), _retrieval_case(s)) for s in (1, 2)]
     # alone, on the default stream
     ref = []
-    rv.set_attention_key_parts(4)
-    try:
-        for (aa, akw), (ra, rkw) in cases:
-            o, lse = rv.biased_chunk_attention(*aa, **akw)
-            ri, rs, rc, _ = rv.retrieve_chunks(*ra, **rkw)
-            torch.cuda.synchronize()
-            ref.append((o.clone(), lse.clone(), ri.clone(), rs.clone(), rc.clone()))
-        errors = []
-
-        def worker(t):
-            try:
-                (aa, akw), (ra, rkw) = cases[t]
-                s = torch.cuda.Stream()
-                with torch.cuda.stream(s):
-                    for _ in range(4):
-                        o, lse = rv.biased_chunk_attention(*aa, **akw)
-                        ri, rs, rc, _ = rv.retrieve_chunks(*ra, **rkw)
-                        s.synchronize()
-                        got = (o, lse, ri, rs, rc)
-                        for name, x, y in zip(("o", "lse", "idx", "score", "count"), got, ref[t]):
-                            if not torch.equal(x, y):
-                                errors.append(f"thread {t}: {name} differs from the result computed alone")
-            except Exception as e:  # reported below
-                errors.append(f"thread {t}: {e!r}")
-
-        threads = [threading.Thread(target=worker, args=(t,)) for t in (0, 1)]
-        for th in threads:
-            th.start()
-        for th in threads:
-            th.join()
+    for (aa, akw), (ra, rkw) in cases:
+        o, lse = rv.biased_chunk_attention(*aa, **akw, key_parts=4)
+        ri, rs, rc, _ = rv.retrieve_chunks(*ra, **rkw)
         torch.cuda.synchronize()
-    finally:
-        rv.set_attention_key_parts(0)
+        ref.append((o.clone(), lse.clone(), ri.clone(), rs.clone(), rc.clone()))
+    errors = []
+
+    def worker(t):
+        try:
+            (aa, akw), (ra, rkw) = cases[t]
+            q, k = aa[0], aa[1]
+            nbytes = max(rv.attention_workspace_size(q.dtype, q.shape[0], k.shape[0], q.shape[1], q.shape[2], 4),
+                         rv.retrieve_workspace_size(ra[0].shape[0], ra[1].shape[0], rkw["k"]))
+            assert nbytes > 0
+            ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                for _ in range(4):
+                    o, lse = rv.biased_chunk_attention(*aa, **akw, key_parts=4, workspace=ws)
+                    ri, rs, rc, _ = rv.retrieve_chunks(*ra, **rkw, workspace=ws)
+                    s.synchronize()
+                    got = (o, lse, ri, rs, rc)
+                    for name, x, y in zip(("o", "lse", "idx", "score", "count"), got, ref[t]):
+                        if not torch.equal(x, y):
+                            errors.append(f"thread {t}: {name} differs from the result computed alone")
+        except Exception as e:  # reported below
+            errors.append(f"thread {t}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in (0, 1)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
     assert not errors, errors

@@ -53,9 +53,9 @@ def _case(rng, Lq, Lk, H, h, w, S):
     return fp8e4m3_bits(q32), fp8e4m3_bits(k32), v, slot, uv, idx, W.bf16_round(q32), W.bf16_round(k32)
 
 
-def _run(q8, k8, v, slot, uv, idx, h, w, scale):
+def _run(q8, k8, v, slot, uv, idx, h, w, scale, key_parts=0):
     return rv.biased_chunk_attention(_fp8_dev(q8), _fp8_dev(k8), dev(v, torch.bfloat16), dev(slot), dev(uv), dev(idx),
-                                     h=h, w=w, softmax_scale=scale, lam=1.0, sigma=2.0)
+                                     h=h, w=w, softmax_scale=scale, lam=1.0, sigma=2.0, key_parts=key_parts)
 
 
 @pytest.mark.parametrize("shape", [(1, 20, 1, 4, 5, 2), (100, 60, 2, 3, 4, 3), (129, 300, 3, 6, 5, 4),
@@ -81,12 +81,8 @@ def test_fp8_qk_key_parts(parts):
     Lq, Lk, H, h, w, S = 300, 40 * 70, 2, 7, 10, 3
     q8, k8, v, slot, uv, idx, _, _ = _case(rng, Lq, Lk, H, h, w, S)
     scale = 1.0 / math.sqrt(128)
-    try:
-        rv.set_attention_key_parts(parts)
-        o, lse = _run(q8, k8, v, slot, uv, idx, h, w, scale)
-        torch.cuda.synchronize()
-    finally:
-        rv.set_attention_key_parts(0)
+    o, lse = _run(q8, k8, v, slot, uv, idx, h, w, scale, key_parts=parts)
+    torch.cuda.synchronize()
     Oo, Lo = OA.biased_attention(OA.fp8e4m3_values(q8), OA.fp8e4m3_values(k8), v, slot, uv, idx, h, w, scale, 1.0, 2.0)
     assert np.abs(host(o) - Oo).max() <= BF16_TOL and np.abs(host(lse) - Lo).max() <= LSE_BF16_TOL
 

@@ -72,13 +72,9 @@ def test_attention_random_sweep(case):
         tol, ltol = BF16_TOL, LSE_BF16_TOL
     print(f"case {case}: {kind} Lq={Lq} Lk={Lk} ({nf} frames of {h}x{w}) H={H} S={S} lam={lam} sigma={sigma:.2f} "
           f"scale={scale:.4f} parts={parts}", flush=True)
-    try:
-        rv.set_attention_key_parts(parts)
-        o, lse = rv.biased_chunk_attention(tq, tk, tv, dev(slot), dev(uv) if S else None, dev(idx) if S else None,
-                                           h=h, w=w, softmax_scale=scale, lam=lam, sigma=sigma)
-        torch.cuda.synchronize()
-    finally:
-        rv.set_attention_key_parts(0)
+    o, lse = rv.biased_chunk_attention(tq, tk, tv, dev(slot), dev(uv) if S else None, dev(idx) if S else None,
+                                       h=h, w=w, softmax_scale=scale, lam=lam, sigma=sigma, key_parts=parts)
+    torch.cuda.synchronize()
     Oo, Lo = OA.biased_attention(q, k, v, slot, uv if S else np.zeros((0, Lq, 2), np.float32),
                                  idx if S else np.zeros((0, Lq), np.int32), h, w, scale, lam, sigma)
     err, lerr = np.abs(host(o) - Oo).max(), np.abs(host(lse) - Lo).max()
