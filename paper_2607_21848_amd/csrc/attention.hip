@@ -17,20 +17,22 @@
 // accumulator registers are 8 consecutive keys, which is the register
 // layout the bf16 B operand wants.
 //
-// The bias on the matrix cores. With centred token coordinates
-// a = u_k - c and u' = u^ - c (c = grid centre) and gamma =
-// lambda / (2 sigma^2 scale),
+// The bias. With gamma = lambda / (2 sigma^2 scale) the biased logit is
+// scale (q.k + (lambda / scale) B), so both kernels put (lambda / scale) B
+// into the logit accumulator before the QK^T MFMAs. The fp32 kernel
+// evaluates it per logit, -gamma |u_k - u^|^2 with the differences taken
+// first. The bf16 kernel uses the separable form: with centred token
+// coordinates a = u_k - c and u' = u^ - c (c = grid centre),
 //     (lambda / scale) B = 2 gamma a.u' - gamma |a|^2 - gamma |u'|^2,
-// a sum of four products of a per-key factor and a per-query factor. Both
-// kernels add it into the logit accumulator with one extra short MFMA per
-// 32-key block that touches a retrieved frame: key side
-// [2 a_x, 2 a_y, -gamma |a|^2, 1], query side [gamma u'_x, gamma u'_y, 1,
-// -gamma |u'|^2], zeroed for keys outside the frame and for rejected
-// queries (so unbiased logits are bit-identical to plain attention). In the
-// bf16 kernel every fp32 factor is split into three bf16 pieces whose sum
-// is the fp32 value exactly; the half-integer a's are exact in bf16. The
-// softmax loop therefore pays nothing for the bias: it is one MFMA per
-// biased 32x32 block next to the eight of the QK^T product.
+// a sum of four products of a per-key factor and a per-query factor, added
+// with one extra MFMA per 32-key block that touches a retrieved frame: key
+// side [2 a_x, 2 a_y, -gamma |a|^2, 1], query side [gamma u'_x, gamma u'_y,
+// 1, -gamma |u'|^2], zeroed for keys outside the frame and for rejected
+// queries (so unbiased logits are bit-identical to plain attention). Every
+// fp32 factor is split into three bf16 pieces whose sum is the fp32 value
+// exactly; the half-integer a's are exact in bf16. The softmax loop
+// therefore pays one MFMA per biased 32x32 block next to the eight of the
+// QK^T product.
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -59,35 +61,6 @@ struct BiasGeom {
     float cx, cy;  // grid centre (w / 2, h / 2)
     int hw, w, h;
 };
-
-// Frame of `key` and its centred token coordinates.
-__device__ __forceinline__ void key_coords(int key, const BiasGeom& g, int& frame, float& ax, float& ay) {
-    frame = key / g.hw;
-    const int t = key - frame * g.hw;
-    const int ky = t / g.w;
-    const int kx = t - ky * g.w;
-    ax = ((float)kx + 0.5f) - g.cx;
-    ay = ((float)ky + 0.5f) - g.cy;
-}
-
-// Per-query bias factors for source frame s: gamma u'_x, gamma u'_y,
-// -gamma |u'|^2; valid = the correspondence was accepted.
-__device__ __forceinline__ void query_factors(const float* corr_uv, const int32_t* corr_idx, int Lq, int s, int q,
-                                              const BiasGeom& g, bool& valid, float& gx, float& gy, float& q0) {
-    valid = false;
-    gx = gy = q0 = 0.0f;
-    if (q < Lq) {
-        const size_t o = (size_t)s * Lq + q;
-        if (corr_idx[o] >= 0) {
-            const float2 u = reinterpret_cast<const float2*>(corr_uv)[o];
-            const float ux = u.x - g.cx, uy = u.y - g.cy;
-            valid = true;
-            gx = g.gamma * ux;
-            gy = g.gamma * uy;
-            q0 = -g.gamma * (ux * ux + uy * uy);
-        }
-    }
-}
 
 // ---------------------------------------------------------------------------
 // fp32 kernel: v_mfma_f32_32x32x2_f32. 4 waves x 32 queries per workgroup,
@@ -120,7 +93,6 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) O[db] = floatx16{0};
     float m_run = -INFINITY, l_run = 0.0f;
-    const int n_frames = a.Lk / g.hw;
 
     for (int tile0 = 0; tile0 < a.Lk; tile0 += TK) {
         __syncthreads();
@@ -133,28 +105,39 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
         }
         __syncthreads();
 
+        // the bias of this lane's 16 logits (query q, keys of rows acc_row(hh, i)),
+        // evaluated directly as -gamma ((u_k,x - u^_x)^2 + (u_k,y - u^_y)^2),
+        // differences first; it is the accumulator's start value
         floatx16 acc = floatx16{0};
-        if (bias_on) {
-            const int k_last = min(tile0 + TK, a.Lk) - 1;
-            const int f0 = tile0 / g.hw, f1 = k_last / g.hw;
-            for (int f = f0; f <= f1 && f < n_frames; ++f) {
-                const int s = a.slot[f];
-                if (s < 0 || s >= a.S) continue;
-                int kf;
-                float ax, ay;
-                const int key = tile0 + n;  // this lane's A-operand row
-                key_coords(key, g, kf, ax, ay);
-                const bool in_f = key <= k_last && kf == f;
-                bool valid;
-                float gx, gy, q0;
-                query_factors(a.corr_uv, a.corr_idx, a.Lq, s, q, g, valid, gx, gy, q0);
-                const float k0 = -g.gamma * (ax * ax + ay * ay);
-                const float a0 = in_f ? (hh ? 2.0f * ay : 2.0f * ax) : 0.0f;
-                const float a1 = in_f ? (hh ? 1.0f : k0) : 0.0f;
-                const float b0 = valid ? (hh ? gy : gx) : 0.0f;
-                const float b1 = valid ? (hh ? q0 : 1.0f) : 0.0f;
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc, 0, 0, 0);
+        if (bias_on && q_ok) {
+            int cf = -1;  // frame whose query factors are loaded
+            bool valid = false;
+            float2 u = make_float2(0.0f, 0.0f);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int key = tile0 + acc_row(hh, i);
+                if (key >= a.Lk) continue;
+                const int f = key / g.hw;
+                if (f != cf) {
+                    cf = f;
+                    const int s = a.slot[f];
+                    valid = false;
+                    if (s >= 0 && s < a.S) {
+                        const size_t o = (size_t)s * a.Lq + q;
+                        if (a.corr_idx[o] >= 0) {
+                            valid = true;
+                            u = reinterpret_cast<const float2*>(a.corr_uv)[o];
+                        }
+                    }
+                }
+                if (valid) {
+                    const int t = key - f * g.hw;
+                    const int ky = t / g.w;
+                    const int kx = t - ky * g.w;
+                    const float dx = ((float)kx + 0.5f) - u.x;
+                    const float dy = ((float)ky + 0.5f) - u.y;
+                    acc[i] = -g.gamma * (dx * dx + dy * dy);
+                }
             }
         }
 #pragma unroll

@@ -222,7 +222,8 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
 // and each thread evaluates v = H u~ for two adjacent tokens, so the launch
 // is a pure write stream of 12 bytes per (token, source). The pair's u^ go
 // out as one 16-byte store and its codes as one 8-byte store where the pair
-// is aligned (the common case), else one token at a time.
+// is aligned (an even element index in outputs whose base addresses are 16-
+// and 8-byte aligned: the common case), else one token at a time.
 struct SrcHomographies {
     double H[kMaxSrcLds][9];
     int status[kMaxSrcLds];  // 0 = use H, else the code of every token (-5, -6)
@@ -324,7 +325,7 @@ __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
                 }
             }
         }
-        if (two && (o & 1) == 0) {
+        if (two && a.paired && (o & 1) == 0) {
             f4 v = {uv[0].x, uv[0].y, uv[1].x, uv[1].y};
             __builtin_nontemporal_store(v, reinterpret_cast<f4*>(a.out_uv + 2 * o));
             i2 c = {code[0], code[1]};
