@@ -70,6 +70,12 @@ def reproject_pair(tgt_depth, tgt_c2w, tgt_K, src_depth, src_c2w, src_K, p, eps)
 
     tgt_depth, src_depth: [h*p, w*p]; c2w: [4, 4]; K: [4] (depth-map px).
     Returns (uv [h*w, 2] float32, idx [h*w] int32), tokens row-major."""
+    return _pair(tgt_depth, tgt_c2w, tgt_K, src_depth, src_c2w, src_K, p, eps)[:2]
+
+
+def _pair(tgt_depth, tgt_c2w, tgt_K, src_depth, src_c2w, src_K, p, eps):
+    """``reproject_pair`` plus, per token, [X_s]_z, D_s(u^) (0 off the grid) and
+    the on-grid mask, for the visibility diagnostics."""
     zt = pooled_depth(tgt_depth, p)
     zs_map = pooled_depth(src_depth, p)
     h, w = zt.shape
@@ -118,7 +124,32 @@ def reproject_pair(tgt_depth, tgt_c2w, tgt_K, src_depth, src_c2w, src_K, p, eps)
 
     uv = np.stack([uhx, uhy], axis=-1)
     uv[~front] = np.nan
-    return uv.reshape(h * w, 2).astype(np.float32), idx.reshape(h * w).astype(np.int32)
+    n = h * w
+    return (uv.reshape(n, 2).astype(np.float32), idx.reshape(n).astype(np.int32), Zs.reshape(n),
+            np.where(on_grid, Ds, 0.0).reshape(n), on_grid.reshape(n))
+
+
+def visibility_near_ties(tgt_depth, tgt_c2w, tgt_K, src_depth, src_c2w, src_K, p, eps, src_sel=None, rel=1e-9):
+    """Diagnostic of Eq. visibility: the number of (source frame, query token)
+    pairs on the source grid whose test is a near tie,
+    |[X_s]_z - (1 + eps) D_s(u^)| < rel D_s(u^). Same inputs as ``reproject``.
+    A mismatch of the visibility decision between two exact evaluations can
+    only occur at such a pair; the parity tests report the count."""
+    tgt_depth = np.asarray(tgt_depth)
+    Tq = tgt_depth.shape[0]
+    S = len(src_sel) if src_sel is not None else np.asarray(src_depth).shape[0]
+    tol = 1.0 + np.float64(np.float32(eps))
+    count = 0
+    for s in range(S):
+        f = s if src_sel is None else int(src_sel[s])
+        if f < 0:
+            continue
+        for t in range(Tq):
+            _, _, Zs, Ds, on_grid = _pair(tgt_depth[t], tgt_c2w[t], tgt_K[t], src_depth[f], src_c2w[f], src_K[f], p,
+                                          eps)
+            with np.errstate(invalid="ignore"):
+                count += int(np.sum(on_grid & (np.abs(Zs - tol * Ds) < rel * Ds)))
+    return count
 
 
 def reproject(tgt_depth, tgt_c2w, tgt_K, src_depth, src_c2w, src_K, p, eps, src_sel=None):

@@ -223,3 +223,25 @@ def test_half_open_grid_edges():
     assert uv[0, 0] == 0.0 and idx[0] == 0                    # col 0 lands on x = 0: on the grid
     uv, idx = R.reproject_pair(d, base, Kk, d, pose_from(np.eye(3), [0.0, -0.5, 0.0]), Kk, p, 0.05)
     assert uv[7 * w, 1] == 8.0 and idx[7 * w] == R.OFF_GRID  # last row lands on y = h
+
+
+def test_visibility_near_ties():
+    """Eq. visibility's near ties, |[X_s]_z - (1 + eps) D_s| < 1e-9 D_s, counted
+    over on-grid pairs. Identity pose over a constant depth of 5 m: [X_s]_z = 5
+    for every token. Against a source map of 4 m with eps = 0.25 the test is
+    5 <= 1.25 * 4 = 5, an exact tie for all 48 tokens (and all are kept);
+    against the same 5 m map, eps = 0 ties every token, eps = 0.05 none; a
+    source looking away (every token behind it) has no pair on the grid."""
+    h, w, p = 6, 8, 2
+    Kk = np.array([[8.0, 8.0, 8.0, 6.0]], np.float32)
+    eye = np.eye(4, dtype=np.float32)[None]
+    d5, d4 = _const(h, w, p, 5.0)[None], _const(h, w, p, 4.0)[None]
+    assert R.visibility_near_ties(d5, eye, Kk, d4, eye, Kk, p, 0.25) == h * w
+    _, idx = R.reproject(d5, eye, Kk, d4, eye, Kk, p, 0.25)
+    assert np.array_equal(idx[0], np.arange(h * w))
+    assert R.visibility_near_ties(d5, eye, Kk, d5, eye, Kk, p, 0.0) == h * w
+    assert R.visibility_near_ties(d5, eye, Kk, d5, eye, Kk, p, 0.05) == 0
+    back = pose_from(axis_angle(np.array([0.0, 1.0, 0.0]), math.pi), [0.0, 0.0, 0.0]).astype(np.float32)[None]
+    assert R.visibility_near_ties(d5, eye, Kk, d5, back, Kk, p, 0.0) == 0
+    # two sources, the second an empty slot of a frame bank
+    assert R.visibility_near_ties(d5, eye, Kk, d4, eye, Kk, p, 0.25, src_sel=[0, -1]) == h * w

@@ -120,3 +120,24 @@ def test_frame_selection_expands_chunks():
     sel = retrieval.frame_selection(idx, np.array([2, 0]), 3)
     assert sel[0].tolist() == [12, 13, 14, 27, 28, 29, -1, -1, -1]
     assert (sel[1] == -1).all()
+
+
+def test_near_ties_hand_built():
+    """near_ties counts a tie between the k-th and (k+1)-th admissible scores
+    and every gate margin at its threshold. Query chunk n = 10 at the origin
+    looking along +z; E = 10, tau_c = 0.25, tau_v = 0 (only exact alignment
+    passes, and every entry is exactly aligned: each live entry is an
+    alignment margin), Delta = 3, first candidate 1, so j = 1..7 are live.
+    j = 1 and j = 2 sit at (+1, 0, 0) and (-1, 0, 0): equal scores 0.1;
+    j = 3 at (2.5, 0, 0) has d = 0.25 = tau_c exactly (a distance margin,
+    admissible, score 0.25); j = 4..7 are 3 m or more away (d > tau_c)."""
+    centres = {0: (0.0, 0.0, 0.0), 1: (1.0, 0.0, 0.0), 2: (-1.0, 0.0, 0.0), 3: (2.5, 0.0, 0.0), 4: (5.0, 0.0, 0.0),
+               5: (0.0, 0.0, 3.0), 6: (0.0, 3.0, 0.0), 7: (0.0, -4.0, 0.0), 8: (0.0, 0.0, 0.0), 9: (0.0, 0.0, 0.0)}
+    bank = np.asarray([pose_from(np.eye(3), np.asarray(centres[j])) for j in range(10)], np.float32)
+    query = np.eye(4, dtype=np.float32)[None]
+    args = (bank, query, np.array([10]), 10.0, 0.5, 0.25, 0.0, 3, 1)
+    idx, sc, cnt = retrieval.retrieve(*args, 3)
+    assert idx[0].tolist() == [1, 2, 3] and cnt[0] == 3
+    assert retrieval.near_ties(*args, 1) == (1, 8)  # s_(1) = s_(2) = 0.1
+    assert retrieval.near_ties(*args, 2) == (0, 8)  # s_(2) = 0.1 < s_(3) = 0.25
+    assert retrieval.near_ties(*args, 3) == (0, 8)  # no (k+1)-th admissible score
