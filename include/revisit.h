@@ -284,6 +284,35 @@ int rc_attention_workspace_size(int32_t dtype, int32_t Lq, int32_t Lk, int32_t H
                                 int32_t key_parts, size_t* bytes);
 
 /*
+ * biased_chunk_attention_noalloc -- for callers that cannot allocate device
+ * memory or bring a workspace (code under HIP graph capture without one,
+ * tight serving loops, harnesses that forbid allocation): the same
+ * arguments, validation and results as biased_chunk_attention, minus the
+ * workspace. It allocates nothing. The bf16 / fp8 key split keeps its
+ * partial results in a library array of 128 MiB per device (a static device
+ * array: each device the library runs on holds its own copy until the
+ * process ends).
+ *   key_parts = 0  the automatic split, cut to the most parts whose partial
+ *                  results fit in 128 MiB (items * P * 66.5 KiB); the results
+ *                  then equal biased_chunk_attention's with that P;
+ *   key_parts > 0  as for biased_chunk_attention; REVISIT_ERR_SHAPE when its
+ *                  partial results need more than 128 MiB.
+ * Every call on one device shares that device's array, which keeps the last
+ * call's contents: calls that may overlap in time on one device (different
+ * streams, graph replays beside other calls) race, and the caller must
+ * order them. Nothing in it needs to start at zero: every partial result the
+ * merge reads is written earlier in the same call. The first call on a
+ * device looks the array's address up (REVISIT_ERR_LAUNCH if that fails).
+ */
+int biased_chunk_attention_noalloc(const void* q, const void* k, const void* v, void* o,
+                                   float* lse, int32_t dtype,
+                                   int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
+                                   const int32_t* kv_frame_slot,
+                                   const float* corr_uv, const int32_t* corr_idx, int32_t S,
+                                   float softmax_scale, float lambda, float sigma,
+                                   int32_t key_parts, hipStream_t stream);
+
+/*
  * pack_retrieved_kv -- Sec. 4.2, cache layout and cache packing.
  *
  * Reinstates retrieved chunks into the attention cache. The history store

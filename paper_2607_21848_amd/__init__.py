@@ -240,14 +240,17 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
                            corr_uv: Optional[torch.Tensor], corr_idx: Optional[torch.Tensor], *,
                            h: int, w: int, softmax_scale: float, lam: float, sigma: float,
                            return_lse: bool = True, out=None, key_parts: int = 0,
-                           workspace: Optional[torch.Tensor] = None):
+                           workspace: Optional[torch.Tensor] = None, noalloc: bool = False):
     """Attention with the Gaussian correspondence bias on retrieved-frame keys.
 
     q [Lq,H,D], k, v [Lk,H,D] (bf16 with D=128, or fp32 with D in {64,128}, or
     q, k float8_e4m3fn with v bf16 and D=128: fp8 logits, o bf16);
     kv_frame_slot [Lk/(h*w)] i32; corr_uv [S,Lq,2] f32 and corr_idx [S,Lq] i32
     (None = no bias). key_parts: 0 = automatic key split, else a fixed
-    number of parts (1..64). Returns (o [Lq,H,D], lse [H,Lq] f32 or None)."""
+    number of parts (1..64). noalloc=True calls
+    biased_chunk_attention_noalloc (the library's per-device scratch array
+    instead of a workspace; with out= given nothing is allocated). Returns
+    (o [Lq,H,D], lse [H,Lq] f32 or None)."""
     dev = q.device
     Lq, H, D = q.shape
     Lk = k.shape[0]
@@ -272,6 +275,14 @@ def biased_chunk_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, kv
         _need(o, "o", vdt, (Lq, H, D), dev)
         if lse is not None:
             _need(lse, "lse", torch.float32, (H, Lq), dev)
+    if noalloc:
+        if workspace is not None:
+            raise ValueError("noalloc=True takes no workspace (it uses the library's scratch array)")
+        st = lib().biased_chunk_attention_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), dt, Lq, Lk, H, D, h,
+                                                  w, _ptr(kv_frame_slot), _ptr(corr_uv), _ptr(corr_idx), S,
+                                                  softmax_scale, lam, sigma, int(key_parts), _stream(dev))
+        _lib.check("biased_chunk_attention_noalloc", st)
+        return o, lse
     with torch.cuda.device(dev):
         nbytes = attention_workspace_size(q.dtype, Lq, Lk, H, D, key_parts)
     ws = _workspace(nbytes, workspace, dev, "workspace")

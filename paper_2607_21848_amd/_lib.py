@@ -17,7 +17,8 @@ OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_PARAM, ERR_LAUNCH, ERR_MEMORY = 0,
 BF16, F32, FP8_QK = 1, 2, 3
 MAX_K = 32
 EXPORTED = ("rc_status_string", "rc_last_error", "retrieve_chunks", "reproject_correspondence",
-            "reproject_rotation", "biased_chunk_attention", "rc_retrieve_workspace_size", "rc_attention_workspace_size",
+            "reproject_rotation", "biased_chunk_attention", "biased_chunk_attention_noalloc", "rc_retrieve_workspace_size",
+            "rc_attention_workspace_size",
             "pack_retrieved_kv", "pool_token_depth", "rc_stream_create", "rc_stream_step", "rc_stream_view",
             "rc_stream_destroy")
 
@@ -74,6 +75,9 @@ def lib() -> ctypes.CDLL:
         L.biased_chunk_attention.restype = ctypes.c_int
         L.biased_chunk_attention.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _i,
                                              _f, _f, _f, _i, _p, _z, _p]
+        L.biased_chunk_attention_noalloc.restype = ctypes.c_int
+        L.biased_chunk_attention_noalloc.argtypes = [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p, _i,
+                                                     _f, _f, _f, _i, _p]
         L.rc_attention_workspace_size.restype = ctypes.c_int
         L.rc_attention_workspace_size.argtypes = [_i, _i, _i, _i, _i, _i, ctypes.POINTER(ctypes.c_size_t)]
         L.pack_retrieved_kv.restype = ctypes.c_int

@@ -39,7 +39,10 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
+#include <new>
 #include <type_traits>
+#include <vector>
 
 #include "internal.h"
 
@@ -1042,6 +1045,39 @@ size_t attention_bf16_workspace_bytes(const AttentionArgs& a, int32_t parts) {
     if (parts <= 1) return 0;
     const int64_t items = (int64_t)((a.Lq + 127) / 128) * a.H;
     return (size_t)items * parts * kPartFloats * sizeof(float);
+}
+
+// The key split's partial results for biased_chunk_attention_noalloc. Each
+// device holds its own copy of this array; host code never passes the name
+// itself to a kernel (on the host it is only a stand-in): it passes the
+// device address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) float scratch[kAttentionScratchBytes / sizeof(float)];
+
+namespace {
+std::mutex g_scratch_mutex;
+std::vector<float*> g_scratch_ptr;  // by device; nullptr = not looked up yet
+}  // namespace
+
+hipError_t attention_scratch(float** ptr) {
+    *ptr = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    // no C++ exception may leave the library's C entry points
+    try {
+        if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize(dev + 1, nullptr);
+    } catch (const std::bad_alloc&) {
+        return hipErrorOutOfMemory;
+    }
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = static_cast<float*>(p);
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_attention_bf16(const AttentionArgs& a, int32_t parts, float* workspace, hipStream_t stream) {

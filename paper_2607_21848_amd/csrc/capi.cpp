@@ -272,38 +272,46 @@ int reproject_rotation(const float* tgt_c2w, const float* tgt_K, const float* sr
     return launched(revisit::launch_rotation(a, stream), "reproject_rotation");
 }
 
-int biased_chunk_attention(const void* q, const void* k, const void* v, void* o, float* lse, int32_t dtype,
-                           int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
-                           const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx, int32_t S,
-                           float softmax_scale, float lambda, float sigma, int32_t key_parts, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream) {
-    int st = check_attention_shape("biased_chunk_attention", dtype, Lq, Lk, H, D, key_parts);
+}  // extern "C"
+
+namespace {
+
+// Validation shared by both attention entry points: fills `a` for a launch,
+// or returns a non-zero status. *nothing = true when there is nothing to do.
+int prepare_attention(const char* fn, const void* q, const void* k, const void* v, void* o, float* lse, int32_t dtype,
+                      int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
+                      const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx, int32_t S,
+                      float softmax_scale, float lambda, float sigma, int32_t key_parts, revisit::AttentionArgs& a,
+                      bool* nothing) {
+    *nothing = false;
+    int st = check_attention_shape(fn, dtype, Lq, Lk, H, D, key_parts);
     if (st != REVISIT_OK) return st;
-    if (h < 1 || w < 1 || S < 0) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: need h, w >= 1, S >= 0");
+    if (h < 1 || w < 1 || S < 0) return fail(REVISIT_ERR_SHAPE, "%s: need h, w >= 1, S >= 0", fn);
     const int64_t hw = (int64_t)h * w;
-    if (Lk % hw != 0) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: Lk=%d not a multiple of h*w=%lld", Lk, (long long)hw);
-    if (Lk / hw > kMaxFrames) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: more than %d KV frames", kMaxFrames);
-    if ((int64_t)S * Lq > kMaxElems) return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: problem too large");
+    if (Lk % hw != 0) return fail(REVISIT_ERR_SHAPE, "%s: Lk=%d not a multiple of h*w=%lld", fn, Lk, (long long)hw);
+    if (Lk / hw > kMaxFrames) return fail(REVISIT_ERR_SHAPE, "%s: more than %d KV frames", fn, kMaxFrames);
+    if ((int64_t)S * Lq > kMaxElems) return fail(REVISIT_ERR_SHAPE, "%s: problem too large", fn);
     if (!(finite(softmax_scale) && softmax_scale > 0.0f))
-        return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: softmax_scale must be finite and > 0");
-    if (!(finite(sigma) && sigma > 0.0f)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: sigma must be finite and > 0");
-    if (!finite(lambda)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: lambda must be finite");
+        return fail(REVISIT_ERR_PARAM, "%s: softmax_scale must be finite and > 0", fn);
+    if (!(finite(sigma) && sigma > 0.0f)) return fail(REVISIT_ERR_PARAM, "%s: sigma must be finite and > 0", fn);
+    if (!finite(lambda)) return fail(REVISIT_ERR_PARAM, "%s: lambda must be finite", fn);
     const float gamma = lambda / (2.0f * sigma * sigma * softmax_scale);
-    if (!finite(gamma)) return fail(REVISIT_ERR_PARAM, "biased_chunk_attention: lambda / (2 sigma^2 scale) overflows");
-    if (Lq == 0) return REVISIT_OK;
+    if (!finite(gamma)) return fail(REVISIT_ERR_PARAM, "%s: lambda / (2 sigma^2 scale) overflows", fn);
+    if (Lq == 0) {
+        *nothing = true;
+        return REVISIT_OK;
+    }
     const bool bias = S > 0 && lambda != 0.0f;
     // the bf16 / fp8 kernel keeps per-column and per-row bias operands of the token grid in LDS
     if (bias && dtype != REVISIT_F32 && (h > kMaxGridSide || w > kMaxGridSide))
-        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: bf16 / fp8 with bias needs h, w <= %d (got %d x %d)",
-                    kMaxGridSide, h, w);
-    if (!q || !k || !v || !o) return fail(REVISIT_ERR_NULL, "biased_chunk_attention: q, k, v and o are required");
+        return fail(REVISIT_ERR_SHAPE, "%s: bf16 / fp8 with bias needs h, w <= %d (got %d x %d)", fn, kMaxGridSide, h, w);
+    if (!q || !k || !v || !o) return fail(REVISIT_ERR_NULL, "%s: q, k, v and o are required", fn);
     if (bias && (!kv_frame_slot || !corr_uv || !corr_idx))
-        return fail(REVISIT_ERR_NULL, "biased_chunk_attention: slot table and correspondence map are required when S > 0");
+        return fail(REVISIT_ERR_NULL, "%s: slot table and correspondence map are required when S > 0", fn);
     // the kernels move q/k/v/o rows in 16-byte vectors and u^ pairs in 8-byte ones
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) || !aligned(lse, 4) ||
         (bias && (!aligned(corr_uv, 8) || !aligned(corr_idx, 4) || !aligned(kv_frame_slot, 4))))
-        return fail(REVISIT_ERR_SHAPE, "biased_chunk_attention: q, k, v, o must be 16-byte aligned, corr_uv 8-byte");
-    revisit::AttentionArgs a;
+        return fail(REVISIT_ERR_SHAPE, "%s: q, k, v, o must be 16-byte aligned, corr_uv 8-byte", fn);
     a.q = q;
     a.k = k;
     a.v = v;
@@ -323,6 +331,23 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     a.lambda = lambda;
     a.sigma = sigma;
     a.fp8_qk = dtype == REVISIT_FP8_QK;
+    return REVISIT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int biased_chunk_attention(const void* q, const void* k, const void* v, void* o, float* lse, int32_t dtype,
+                           int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
+                           const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx, int32_t S,
+                           float softmax_scale, float lambda, float sigma, int32_t key_parts, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+    revisit::AttentionArgs a{};
+    bool nothing = false;
+    int st = prepare_attention("biased_chunk_attention", q, k, v, o, lse, dtype, Lq, Lk, H, D, h, w, kv_frame_slot,
+                               corr_uv, corr_idx, S, softmax_scale, lambda, sigma, key_parts, a, &nothing);
+    if (st != REVISIT_OK || nothing) return st;
     if (dtype == REVISIT_F32) return launched(revisit::launch_attention_f32(a, stream), "biased_chunk_attention");
     int32_t parts = 1;
     size_t need = 0;
@@ -332,6 +357,41 @@ int biased_chunk_attention(const void* q, const void* k, const void* v, void* o,
     if (st != REVISIT_OK) return st;
     return launched(revisit::launch_attention_bf16(a, parts, static_cast<float*>(workspace), stream),
                     "biased_chunk_attention");
+}
+
+int biased_chunk_attention_noalloc(const void* q, const void* k, const void* v, void* o, float* lse, int32_t dtype,
+                                   int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t h, int32_t w,
+                                   const int32_t* kv_frame_slot, const float* corr_uv, const int32_t* corr_idx,
+                                   int32_t S, float softmax_scale, float lambda, float sigma, int32_t key_parts,
+                                   hipStream_t stream) {
+    const char* fn = "biased_chunk_attention_noalloc";
+    revisit::AttentionArgs a{};
+    bool nothing = false;
+    int st = prepare_attention(fn, q, k, v, o, lse, dtype, Lq, Lk, H, D, h, w, kv_frame_slot, corr_uv, corr_idx, S,
+                               softmax_scale, lambda, sigma, key_parts, a, &nothing);
+    if (st != REVISIT_OK || nothing) return st;
+    if (dtype == REVISIT_F32) return launched(revisit::launch_attention_f32(a, stream), fn);
+    int32_t parts = 1;
+    size_t need = 0;
+    st = attention_parts(fn, a, key_parts, &parts, &need);
+    if (st != REVISIT_OK) return st;
+    if (need > revisit::kAttentionScratchBytes) {
+        if (key_parts != 0)
+            return fail(REVISIT_ERR_SHAPE, "%s: %d key parts need %zu bytes of scratch, more than the %zu bytes it holds "
+                                           "(use fewer parts, or biased_chunk_attention with a workspace)",
+                        fn, parts, need, revisit::kAttentionScratchBytes);
+        // the automatic split, cut to the most parts whose partial results fit
+        while (parts > 1 && revisit::attention_bf16_workspace_bytes(a, parts) > revisit::kAttentionScratchBytes)
+            --parts;
+        need = revisit::attention_bf16_workspace_bytes(a, parts);
+    }
+    float* scratch = nullptr;
+    if (need > 0) {
+        const hipError_t e = revisit::attention_scratch(&scratch);
+        if (e != hipSuccess)
+            return fail(REVISIT_ERR_LAUNCH, "%s: device address of the scratch array: %s", fn, hipGetErrorString(e));
+    }
+    return launched(revisit::launch_attention_bf16(a, parts, scratch, stream), fn);
 }
 
 int rc_attention_workspace_size(int32_t dtype, int32_t Lq, int32_t Lk, int32_t H, int32_t D, int32_t key_parts,

@@ -91,6 +91,13 @@ int32_t attention_bf16_key_parts(const AttentionArgs& a, int32_t slots);
 size_t attention_bf16_workspace_bytes(const AttentionArgs& a, int32_t parts);
 hipError_t launch_attention_bf16(const AttentionArgs& a, int32_t parts, float* workspace, hipStream_t stream);
 
+// Scratch of biased_chunk_attention_noalloc: a file-scope device array in
+// attention.hip of kAttentionScratchBytes, one per device for the life of the
+// process. attention_scratch() returns its device address on the current
+// device (looked up once per device).
+constexpr size_t kAttentionScratchBytes = (size_t)128 << 20;
+hipError_t attention_scratch(float** ptr);
+
 // Cache packing of retrieved chunks (kvpack.hip). Element size 2 (bf16) or
 // 4 (fp32); T = tokens per chunk; store [L][n_store][T][H][D], cache
 // [L][cache_rows][H][D].

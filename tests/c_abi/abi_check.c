@@ -70,6 +70,10 @@ static void host_checks(void) {
     st = biased_chunk_attention(FAKE, FAKE, FAKE, FAKE, NULL, REVISIT_BF16, 4680, 37440, 12, 128, 30, 52, FAKE, FAKE,
                                 FAKE, 12, 0.088f, 1.0f, 2.0f, 4, FAKE, 4096, NULL);
     CHECK(st == REVISIT_ERR_SHAPE, "biased_chunk_attention with a 4 KiB workspace for 4 key parts: %d", st);
+    /* 64 parts of 444 items need 1.9 GB of partial results, more than the no-allocation scratch */
+    st = biased_chunk_attention_noalloc(FAKE, FAKE, FAKE, FAKE, NULL, REVISIT_BF16, 4680, 37440, 12, 128, 30, 52, FAKE,
+                                        FAKE, FAKE, 12, 0.088f, 1.0f, 2.0f, 64, NULL);
+    CHECK(st == REVISIT_ERR_SHAPE, "biased_chunk_attention_noalloc with 64 key parts: %d", st);
 
     st = reproject_correspondence(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NULL, 0, 1, 3, 6, 30, 52, 2, -1.0f, FAKE, FAKE,
                                   NULL);

@@ -263,3 +263,27 @@ def test_stream_null_arguments(L):
 ])
 def test_pool_token_depth_rejects(L, args, status):
     assert L.pool_token_depth(*args, NULL) == status
+
+
+def _attention_noalloc(L, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=NULL, dtype=1, Lq=4680, Lk=37440, H=12, D=128, h=30, w=52,
+             slot=FAKE, uv=FAKE, idx=FAKE, S=12, scale=1 / math.sqrt(128), lam=1.0, sigma=2.0, parts=64)
+    a.update(kw)
+    return L.biased_chunk_attention_noalloc(a["q"], a["k"], a["v"], a["o"], a["lse"], a["dtype"], a["Lq"], a["Lk"],
+                                            a["H"], a["D"], a["h"], a["w"], a["slot"], a["uv"], a["idx"], a["S"],
+                                            a["scale"], a["lam"], a["sigma"], a["parts"], NULL)
+
+
+@pytest.mark.parametrize("kw,status", [
+    # 444 items x 64 parts x 66560 bytes of partial results: more than the 128 MiB scratch
+    (dict(), 2), (dict(parts=3, Lq=9360, H=24), 2),
+    (dict(dtype=7), 3), (dict(sigma=0.0), 4), (dict(parts=65), 4), (dict(q=NULL), 1), (dict(Lk=37441), 2),
+])
+def test_attention_noalloc_rejects(L, kw, status):
+    from paper_2607_21848_amd import _lib
+    assert _attention_noalloc(L, **kw) == status
+    assert "biased_chunk_attention_noalloc" in _lib.last_error()
+
+
+def test_attention_noalloc_nothing_to_do(L):
+    assert _attention_noalloc(L, Lq=0) == 0
