@@ -16,8 +16,13 @@ last-level cache), retrieval latency, the retrieval bandwidth on a stress
 bank, and the cache packing of the step's retrieved chunks for all 30
 layers from a store of every bank chunk's keys and values (HBM-bound, not
 part of the step), and the streaming driver's per-chunk time for the paper's
-cache layout over all 30 layers; ``cpu_baseline`` times the fp64
-oracle on a bounded sample of the same workload on this host.
+cache layout over all 30 layers; ``configs`` times every workload
+configuration at its own shape (C1 tiny fp32 reference, C2 plain window with
+the bias off, C3 loop closure, C4 the headline's history bank, C5 Wan-14B
+720p): attention with the bias on and off, fp8 logits with their deviation
+from the bf16 output, and the configuration's correspondence and retrieval,
+each next to the fp64 oracle timed on a sample; ``cpu_baseline`` times the
+fp64 oracle on a bounded sample of the headline workload on this host.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -41,6 +46,7 @@ if ROOT not in sys.path:
 METRIC = "biased-attention TFLOP/s + MFMA util; reprojection tokens/s (Wan-1.3B shape)"
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+FP32_PEAK_TFLOPS = 157.3  # MI355X fp32 (the fp32 attention kernel runs on the fp32 matrix cores)
 FP8_BF16_PEAK_TFLOPS = 2.0 / (1.0 / 5000.0 + 1.0 / 2500.0)  # half the flops at the fp8 peak, half at bf16
 BENCH_QUERY = 1  # query chunk n = 225: a full top-4 retrieval
 PACK_LAYERS = 30  # transformer blocks of the 1.3B backbone: one packing call covers all of them
@@ -398,6 +404,10 @@ def main():
         f"Lk {int(np.median(s_lk))}, attention {stream_flops / (stream_ms * 1e-3) / 1e12:.1f} TFLOP/s over the chunk")
     del sq, sk, sv, so, slse, s_in
 
+    log("sweep over the five workload configurations")
+    configs = config_sweep(dev, stream, ws, q, k, v, slot, cuv, cidx, o, lse, wl, attn_ms, a8_ms, a8_dev,
+                           retr_ms, repr_ms, not args.no_cpu_baseline)
+
     counters = profiled_counters()
     out = {
         "metric": METRIC,
@@ -488,6 +498,8 @@ def main():
         },
     }
 
+    out["configs"] = configs
+
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -501,6 +513,245 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def _timed(fn, reps, stream):
+    """Mean milliseconds per call of fn over `reps` back-to-back calls (after two
+    warm-up calls), from HIP events recorded on the launch stream."""
+    import torch
+    for _ in range(2):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _attn_entry(flops, ms_on, ms_off, peak, dtype):
+    e = {"dtype": dtype, "flops_per_call": flops, "peak_tflops": peak}
+    for tag, ms in (("bias_on", ms_on), ("bias_off", ms_off)):
+        if ms is not None:
+            e[f"ms_{tag}"] = round(ms, 4)
+            e[f"tflops_{tag}"] = round(flops / (ms * 1e-3) / 1e12, 2)
+            e[f"frac_{tag}"] = round(flops / (ms * 1e-3) / 1e12 / peak, 4)
+    return e
+
+
+def _oracle_attention_sample(qv, kv, vv, slot, uv, idx, wl, n_rows):
+    """Seconds the fp64 oracle takes for n_rows sampled query rows (all heads),
+    and the attention flops that covers."""
+    from oracle import attention as OA
+    rows = np.linspace(0, wl.Lq - 1, n_rows).astype(np.int64)
+    t0 = time.perf_counter()
+    OA.biased_attention(qv, kv, vv, slot, uv, idx, wl.h, wl.w, wl.softmax_scale, wl.lam, wl.sigma, rows=rows,
+                        block=n_rows)
+    dt = time.perf_counter() - t0
+    return dt, 4.0 * n_rows * wl.Lk * wl.D * wl.H
+
+
+def config_sweep(dev, stream, ws, q4, k4, v4, slot4, cuv4, cidx4, o4, lse4, wl4, attn4_ms, a8_4_ms, a8_4_dev,
+                 retr4_ms, repr4_ms, with_oracle):
+    """Every workload configuration at its own shape: attention with the bias on
+    and off (fp32 for the tiny reference, bf16 otherwise, plus fp8 logits where
+    the configuration has retrieved frames), and the configuration's
+    correspondence and retrieval, each timed with HIP events; where asked, the
+    fp64 oracle timed on a sample of the same inputs. Q, K and V of the
+    Wan-shaped configurations are drawn N(0, 1) on the device (seeded)."""
+    import torch
+
+    import paper_2607_21848_amd as rv
+    import workloads as W
+    from oracle import reprojection as OR, retrieval as ORT
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    gen = torch.Generator(device=dev)
+    threads = blas_threads()
+    res = {}
+
+    def randn_bf16(shape, seed):
+        gen.manual_seed(seed)
+        return torch.randn(shape, generator=gen, device=dev).to(torch.bfloat16)
+
+    def host64(x):
+        return x.float().cpu().numpy()
+
+    def attn_call(wl, q, k, v, slot, uv, idx, lam, o, lse):
+        return lambda: rv.biased_chunk_attention(q, k, v, slot, uv, idx, h=wl.h, w=wl.w,
+                                                 softmax_scale=wl.softmax_scale, lam=lam, sigma=wl.sigma,
+                                                 out=(o, lse), workspace=ws)
+
+    def fp8_entry(wl, q, k, v, slot, uv, idx, o_ref, reps):
+        q8, k8 = q.float().to(torch.float8_e4m3fn), k.float().to(torch.float8_e4m3fn)
+        o8, l8 = torch.empty_like(o_ref), torch.empty((wl.H, wl.Lq), dtype=torch.float32, device=dev)
+        ms = _timed(attn_call(wl, q8, k8, v, slot, uv, idx, wl.lam, o8, l8), reps, stream)
+        d = (o8.float() - o_ref.float()).abs()
+        e = _attn_entry(wl.flops, ms, None, FP8_BF16_PEAK_TFLOPS, "fp8 q, k; bf16 v, o")
+        e["max_abs_dev_from_bf16_output"] = float(d.max().item())
+        e["mean_abs_dev_from_bf16_output"] = float(d.mean().item())
+        return e
+
+    # C1: tiny fp32 reference, full oracle
+    wl = W.make_c1()
+    log("config C1 (tiny fp32 reference)")
+    tgt = [t(a) for a in (wl.tgt_depth, wl.tgt_c2w, wl.tgt_K)]
+    src = [t(a) for a in (wl.src_depth, wl.src_c2w, wl.src_K)]
+    uv = torch.empty((1, wl.S, wl.Lq, 2), dtype=torch.float32, device=dev)
+    idx = torch.empty((1, wl.S, wl.Lq), dtype=torch.int32, device=dev)
+    r_ms = _timed(lambda: rv.reproject_correspondence(*tgt, *src, p=wl.p, eps=wl.eps, out=(uv, idx)), 50, stream)
+    q, k, v, slot = t(wl.q), t(wl.k), t(wl.v), t(wl.slot)
+    o = torch.empty_like(q)
+    lse = torch.empty((wl.H, wl.Lq), dtype=torch.float32, device=dev)
+    on = _timed(attn_call(wl, q, k, v, slot, uv[0], idx[0], wl.lam, o, lse), 50, stream)
+    off = _timed(attn_call(wl, q, k, v, slot, None, None, 0.0, o, lse), 50, stream)
+    e = {"workload": W.CONFIG_NAMES[1], "attention": _attn_entry(wl.flops, on, off, FP32_PEAK_TFLOPS, "f32"),
+         "reprojection": {"us": round(r_ms * 1e3, 2), "tokens": wl.Lq, "sources": wl.S,
+                          "tokens_per_s": round(wl.Lq / (r_ms * 1e-3), 0)}}
+    if with_oracle:
+        from oracle import attention as OA
+        t0 = time.perf_counter()
+        ouv, oidx = OR.reproject(wl.tgt_depth, wl.tgt_c2w, wl.tgt_K, wl.src_depth, wl.src_c2w, wl.src_K, wl.p, wl.eps)
+        t1 = time.perf_counter()
+        OA.biased_attention(wl.q, wl.k, wl.v, wl.slot, ouv, oidx, wl.h, wl.w, wl.softmax_scale, wl.lam, wl.sigma)
+        t2 = time.perf_counter()
+        e["oracle"] = {"kind": "oracle", "cores": threads, "sample": "the whole configuration",
+                       "reprojection_s": round(t1 - t0, 4), "attention_s": round(t2 - t1, 4),
+                       "attention_tflops": round(wl.flops / (t2 - t1) / 1e12, 6)}
+    res["C1"] = e
+
+    # C2: plain window, no retrieved frames (bias off)
+    wl = W.make_c2("bf16", qkv=False)
+    log("config C2 (Wan-1.3B plain window, bias off)")
+    q = randn_bf16((wl.Lq, wl.H, wl.D), 201)
+    k = randn_bf16((wl.Lk, wl.H, wl.D), 202)
+    v = randn_bf16((wl.Lk, wl.H, wl.D), 203)
+    slot = t(wl.slot)
+    o = torch.empty_like(q)
+    lse = torch.empty((wl.H, wl.Lq), dtype=torch.float32, device=dev)
+    off = _timed(attn_call(wl, q, k, v, slot, None, None, 0.0, o, lse), 10, stream)
+    e = {"workload": W.CONFIG_NAMES[2], "attention": _attn_entry(wl.flops, None, off, BF16_PEAK_TFLOPS, "bf16")}
+    if with_oracle:
+        dt, fl = _oracle_attention_sample(host64(q), host64(k), host64(v), wl.slot, None, None, wl, 8)
+        e["oracle"] = {"kind": "oracle", "cores": threads, "sample": "8 query rows, all heads and keys",
+                       "attention_s": round(dt, 3), "attention_tflops": round(fl / dt / 1e12, 6)}
+    res["C2"] = e
+    del q, k, v, o
+
+    # C3: loop closure with fixed retrieved frames
+    wl = W.make_c3("bf16", qkv=False)
+    log("config C3 (Wan-1.3B loop closure)")
+    tgt = [t(a[None]) for a in (wl.tgt_depth, wl.tgt_c2w, wl.tgt_K)]
+    src = [t(a[None]) for a in (wl.src_depth, wl.src_c2w, wl.src_K)]
+    uv = torch.empty((1, wl.S, wl.Lq, 2), dtype=torch.float32, device=dev)
+    idx = torch.empty((1, wl.S, wl.Lq), dtype=torch.int32, device=dev)
+    r_ms = _timed(lambda: rv.reproject_correspondence(*tgt, *src, p=wl.p, eps=wl.eps, out=(uv, idx)), 50, stream)
+    q = randn_bf16((wl.Lq, wl.H, wl.D), 301)
+    k = randn_bf16((wl.Lk, wl.H, wl.D), 302)
+    v = randn_bf16((wl.Lk, wl.H, wl.D), 303)
+    slot = t(wl.slot)
+    o = torch.empty_like(q)
+    lse = torch.empty((wl.H, wl.Lq), dtype=torch.float32, device=dev)
+    off = _timed(attn_call(wl, q, k, v, slot, None, None, 0.0, o, lse), 10, stream)
+    on = _timed(attn_call(wl, q, k, v, slot, uv[0], idx[0], wl.lam, o, lse), 10, stream)
+    in_bounds = float((idx[0] >= 0).float().mean().item())
+    e = {"workload": W.CONFIG_NAMES[3], "attention": _attn_entry(wl.flops, on, off, BF16_PEAK_TFLOPS, "bf16"),
+         "attention_fp8_logits": fp8_entry(wl, q, k, v, slot, uv[0], idx[0], o, 10),
+         "reprojection": {"us": round(r_ms * 1e3, 2), "tokens": wl.Lq, "sources": wl.S,
+                          "tokens_per_s": round(wl.Lq / (r_ms * 1e-3), 0), "accepted_fraction": round(in_bounds, 4)}}
+    if with_oracle:
+        t0 = time.perf_counter()
+        ouv, oidx = OR.reproject(wl.tgt_depth, wl.tgt_c2w, wl.tgt_K, wl.src_depth, wl.src_c2w, wl.src_K, wl.p, wl.eps)
+        t1 = time.perf_counter()
+        dt, fl = _oracle_attention_sample(host64(q), host64(k), host64(v), wl.slot, ouv, oidx, wl, 8)
+        e["oracle"] = {"kind": "oracle", "cores": threads, "sample": "reprojection of the chunk; attention for 8 "
+                       "query rows, all heads and keys", "reprojection_s": round(t1 - t0, 3),
+                       "attention_s": round(dt, 3), "attention_tflops": round(fl / dt / 1e12, 6)}
+    res["C3"] = e
+    del q, k, v, o
+
+    # C4: the headline step's shape; bias off measured here
+    log("config C4 (Wan-1.3B history bank, the headline step)")
+    off = _timed(attn_call(wl4, q4, k4, v4, slot4, None, None, 0.0, o4, lse4), 10, stream)
+    e8 = _attn_entry(wl4.flops, a8_4_ms, None, FP8_BF16_PEAK_TFLOPS, "fp8 q, k; bf16 v, o")
+    e8["max_abs_dev_from_bf16_output"] = a8_4_dev
+    res["C4"] = {"workload": W.CONFIG_NAMES[4],
+                 "attention": _attn_entry(wl4.flops, attn4_ms, off, BF16_PEAK_TFLOPS, "bf16"),
+                 "attention_fp8_logits": e8,
+                 "retrieval_us": round(retr4_ms * 1e3, 2), "reprojection_us": round(repr4_ms * 1e3, 2),
+                 "note": "bias-on, fp8, retrieval and reprojection times are the headline step's"}
+
+    # C5: Wan-14B 720p with top-2 retrieval from a 300-chunk bank
+    wl = W.make_c5("bf16", qkv=False)
+    r = wl.retrieval
+    log("config C5 (Wan-14B 720p)")
+    bank_c2w, q_c2w, q_chunk = t(r.bank_c2w), t(r.query_c2w[:1]), t(r.query_chunk[:1])
+    bank = [t(a) for a in (r.bank_frame_depth, r.bank_frame_c2w, r.bank_frame_K)]
+    tgt = [t(a[:1]) for a in (r.query_frame_depth, r.query_frame_c2w, r.query_frame_K)]
+    ridx = torch.empty((1, r.k), dtype=torch.int32, device=dev)
+    rscore = torch.empty((1, r.k), dtype=torch.float32, device=dev)
+    rcount = torch.empty((1,), dtype=torch.int32, device=dev)
+    rsel = torch.empty((1, r.k * 3), dtype=torch.int32, device=dev)
+    uv = torch.empty((1, wl.S, wl.Lq, 2), dtype=torch.float32, device=dev)
+    idx = torch.empty((1, wl.S, wl.Lq), dtype=torch.int32, device=dev)
+    rt_ms = _timed(lambda: rv.retrieve_chunks(bank_c2w, q_c2w, q_chunk, E=r.E, w_v=r.w_v, tau_c=r.tau_c,
+                                              tau_v=r.tau_v, delta=r.delta, first_candidate=r.first_candidate,
+                                              k=r.k, frames_per_chunk=3, out=(ridx, rscore, rcount, rsel)),
+                   50, stream)
+    r_ms = _timed(lambda: rv.reproject_correspondence(*tgt, *bank, p=wl.p, eps=wl.eps, src_sel=rsel,
+                                                      out=(uv, idx)), 50, stream)
+    q = randn_bf16((wl.Lq, wl.H, wl.D), 501)
+    k = randn_bf16((wl.Lk, wl.H, wl.D), 502)
+    v = randn_bf16((wl.Lk, wl.H, wl.D), 503)
+    slot = t(wl.slot)
+    o = torch.empty_like(q)
+    lse = torch.empty((wl.H, wl.Lq), dtype=torch.float32, device=dev)
+    ws5 = torch.empty(max(rv.attention_workspace_size(torch.bfloat16, wl.Lq, wl.Lk, wl.H, wl.D),
+                          rv.attention_workspace_size(torch.float8_e4m3fn, wl.Lq, wl.Lk, wl.H, wl.D), 16),
+                      dtype=torch.uint8, device=dev)
+
+    def attn5(lam, uv_, idx_, qq=q, kk=k, oo=o, ll=lse):
+        return lambda: rv.biased_chunk_attention(qq, kk, v, slot, uv_, idx_, h=wl.h, w=wl.w,
+                                                 softmax_scale=wl.softmax_scale, lam=lam, sigma=wl.sigma,
+                                                 out=(oo, ll), workspace=ws5)
+    off = _timed(attn5(0.0, None, None), 5, stream)
+    on = _timed(attn5(wl.lam, uv[0], idx[0]), 5, stream)
+    q8, k8 = q.float().to(torch.float8_e4m3fn), k.float().to(torch.float8_e4m3fn)
+    o8, l8 = torch.empty_like(o), torch.empty_like(lse)
+    on8 = _timed(attn5(wl.lam, uv[0], idx[0], q8, k8, o8, l8), 5, stream)
+    d8 = (o8.float() - o.float()).abs()
+    e8 = _attn_entry(wl.flops, on8, None, FP8_BF16_PEAK_TFLOPS, "fp8 q, k; bf16 v, o")
+    e8["max_abs_dev_from_bf16_output"] = float(d8.max().item())
+    e8["mean_abs_dev_from_bf16_output"] = float(d8.mean().item())
+    del q8, k8, o8
+    e = {"workload": W.CONFIG_NAMES[5], "attention": _attn_entry(wl.flops, on, off, BF16_PEAK_TFLOPS, "bf16"),
+         "attention_fp8_logits": e8, "retrieval_us": round(rt_ms * 1e3, 2),
+         "retrieved": ridx[0].tolist(),
+         "reprojection": {"us": round(r_ms * 1e3, 2), "tokens": wl.Lq, "sources": wl.S,
+                          "tokens_per_s": round(wl.Lq / (r_ms * 1e-3), 0),
+                          "accepted_fraction": round(float((idx[0] >= 0).float().mean().item()), 4)}}
+    if with_oracle:
+        t0 = time.perf_counter()
+        oi, _, oc = ORT.retrieve(r.bank_c2w, r.query_c2w[:1], r.query_chunk[:1], r.E, r.w_v, r.tau_c, r.tau_v,
+                                 r.delta, r.first_candidate, r.k)
+        sel = ORT.frame_selection(oi, oc, 3)[0]
+        t1 = time.perf_counter()
+        ouv, oidx = OR.reproject(r.query_frame_depth[0], r.query_frame_c2w[0], r.query_frame_K[0],
+                                 r.bank_frame_depth, r.bank_frame_c2w, r.bank_frame_K, wl.p, wl.eps, src_sel=sel)
+        t2 = time.perf_counter()
+        dt, fl = _oracle_attention_sample(host64(q), host64(k), host64(v), wl.slot, ouv, oidx, wl, 4)
+        e["oracle"] = {"kind": "oracle", "cores": threads, "sample": "retrieval and reprojection of the chunk; "
+                       "attention for 4 query rows, all heads and keys", "retrieval_s": round(t1 - t0, 4),
+                       "reprojection_s": round(t2 - t1, 3), "attention_s": round(dt, 3),
+                       "attention_tflops": round(fl / dt / 1e12, 6)}
+    res["C5"] = e
+    del q, k, v, o, ws5
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(wl, target_s):

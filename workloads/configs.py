@@ -190,11 +190,11 @@ def make_c1() -> Workload:
 # --------------------------------------------------------------------------
 # C2: Wan-1.3B plain window (bias off)
 # --------------------------------------------------------------------------
-def make_c2(dtype: str = "bf16") -> Workload:
+def make_c2(dtype: str = "bf16", qkv: bool = True) -> Workload:
     rng = _rng(2)
     h, w = 30, 52
     hw = h * w
-    q, k, v = _qkv(rng, 3 * hw, 12 * hw, 12, 128, dtype)
+    q, k, v = _qkv(rng, 3 * hw, 12 * hw, 12, 128, dtype) if qkv else (None, None, None)
     return Workload(
         config_id=2, name=CONFIG_NAMES[2], dtype=dtype, H=12, D=128, h=h, w=w, p=2, Tq=3,
         Lq=3 * hw, Lk=12 * hw, slot=np.full(12, -1, np.int32), S=0,
@@ -230,14 +230,14 @@ def make_c3_geometry(rng, h=30, w=52, p=2):
     )
 
 
-def make_c3(dtype: str = "bf16") -> Workload:
+def make_c3(dtype: str = "bf16", qkv: bool = True) -> Workload:
     rng = _rng(3)
     h, w, p = 30, 52, 2
     hw = h * w
     geo = make_c3_geometry(rng, h, w, p)
     slot = np.full(18, -1, np.int32)
     slot[3:9] = np.arange(6)
-    q, k, v = _qkv(rng, 3 * hw, 18 * hw, 12, 128, dtype)
+    q, k, v = _qkv(rng, 3 * hw, 18 * hw, 12, 128, dtype) if qkv else (None, None, None)
     return Workload(
         config_id=3, name=CONFIG_NAMES[3], dtype=dtype, H=12, D=128, h=h, w=w, p=p, Tq=3,
         Lq=3 * hw, Lk=18 * hw, slot=slot, S=6,
