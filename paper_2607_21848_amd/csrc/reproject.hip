@@ -16,6 +16,11 @@
 // Arithmetic is IEEE double in the order of the definition with
 // contraction disabled; the code and u^ (rounded to fp32 once) are
 // therefore bit-identical to any IEEE evaluation of the same expressions.
+// The quotients are the IEEE ones: where every input lies in a range that
+// keeps all intermediates normal (checked per block and per wave), the two
+// coordinates of u^ share one correctly rounded reciprocal of [X_s]_z and
+// take one Markstein correction each (quotient.h), which equals the IEEE
+// quotient there; elsewhere the kernel divides.
 // For the usual p = 2 the kernel is specialised: dividing by 2 or by 4 is
 // the same IEEE result as multiplying by 0.5 or 0.25, so the token-grid
 // intrinsics and the pooling mean cost a multiply instead of a division,
@@ -27,6 +32,7 @@
 #include <stdint.h>
 
 #include "internal.h"
+#include "quotient.h"
 
 #pragma clang fp contract(off)
 
@@ -90,39 +96,95 @@ struct Corr {
     int code;
 };
 
-// Source frame s of the block's problem, converted to doubles in LDS:
-// R (row-major), c, token-grid (fx, fy, cx, cy); frame index -1 = no source.
+// Frames of the block's problem converted to doubles in LDS: per source s,
+// R (row-major), c, token-grid (fx, fy, cx, cy), and its frame index (-1 = no
+// source); the same 16 values of the block's target frame in tc, and the
+// correctly rounded reciprocals of its fx and fy in trcp.
 struct SrcFrames {
     double c[kMaxSrcLds][16];
     int f[kMaxSrcLds];
+    double tc[16];
+    double trcp[2];
+    int out_of_range[kBlock / 64];  // per wave: a frame value outside the shared-reciprocal range
 };
 
+// The 16 doubles of a frame: R row-major, c, then K / p on the token grid.
 template <int P>
-__device__ __forceinline__ Lifted lift(double z, int i, int j, double fxt, double fyt, double cxt, double cyt,
-                                       const float* Mt) {
+__device__ __forceinline__ double frame_value(const float* M, const float* K, int v, double pd) {
+    if (v < 9) return (double)M[4 * (v / 3) + v % 3];
+    if (v < 12) return (double)M[4 * (v - 9) + 3];
+    return per_token<P>(K[v - 12], pd);
+}
+
+// Range condition of the shared-reciprocal quotients (quotient.h) on a frame
+// value: zero or of magnitude in [2^-64, 2^64]; fx and fy (v = 12, 13)
+// nonzero; cx and cy (v = 14, 15) not -0. With every frame value of a problem
+// in range and the target depth z in [2^-40, 2^40], every quantity the
+// correspondence computes is zero or of magnitude in [2^-850, 2^800]: the
+// operands are products of a few in-range factors (numerators at least
+// 2^-540, denominators in [2^-423, 2^302]), every nonzero sum is a multiple
+// of the smallest unit of its terms, and the quotients' residuals are
+// multiples of 2^-644. The quotients' intermediates therefore stay normal and
+// no numerator is -0, so the shared-reciprocal quotient is the IEEE one.
+__device__ __forceinline__ bool frame_value_in_range(double x, int v) {
+    const double m = fabs(x);
+    const bool mag = m >= 0x1p-64 && m <= 0x1p64;
+    if (v == 12 || v == 13) return mag;
+    if (v >= 14 && x == 0.0 && signbit(x)) return false;
+    return x == 0.0 || mag;
+}
+
+// X_t = z K_t^-1 u~ lifted to the world: R_t X_t + c_t (the source centre
+// comes later). T holds the target frame's 16 doubles, Trcp 1 / fx, 1 / fy;
+// kShared selects the shared-reciprocal quotients.
+template <bool kShared>
+__device__ __forceinline__ Lifted lift(double z, int i, int j, const double* T, const double* Trcp) {
     Lifted L;
     L.defined = isfinite(z) && z > 0.0;
-    // X_t = z K_t^-1 u~, then R_t X_t + c_t (the source centre comes later)
     const double ux = (double)j + 0.5, uy = (double)i + 0.5;
-    const double Xt = ((ux - cxt) / fxt) * z;
-    const double Yt = ((uy - cyt) / fyt) * z;
+    double qx, qy;
+    if constexpr (kShared) {
+        qx = quotient_from_reciprocal(ux - T[14], T[12], Trcp[0]);
+        qy = quotient_from_reciprocal(uy - T[15], T[13], Trcp[1]);
+    } else {
+        qx = (ux - T[14]) / T[12];
+        qy = (uy - T[15]) / T[13];
+    }
+    const double Xt = qx * z;
+    const double Yt = qy * z;
     const double Zt = z;
 #pragma unroll
-    for (int r = 0; r < 3; ++r) {
-        L.W[r] = (((double)Mt[4 * r + 0] * Xt + (double)Mt[4 * r + 1] * Yt) + (double)Mt[4 * r + 2] * Zt) +
-                 (double)Mt[4 * r + 3];
-    }
+    for (int r = 0; r < 3; ++r) L.W[r] = ((T[3 * r + 0] * Xt + T[3 * r + 1] * Yt) + T[3 * r + 2] * Zt) + T[9 + r];
     return L;
 }
 
-// Eq. reprojection and Eq. visibility for one (lifted token, source frame s).
+// Pooled depth of cell (i, j) of a source frame whose base is uniform across
+// the wave; the in-frame byte offset fits in 32 bits (a frame holds at most
+// 2^28 pixels).
 template <int P>
-__device__ __forceinline__ Corr correspond(const ReprojectArgs& a, const Lifted& L, const SrcFrames& sf, int s, int Wd,
-                                           size_t frame_px, int p, double tol) {
-    const int f = sf.f[s];
-    if (f < 0) return Corr{make_float2(NAN, NAN), -5};
-    if (!L.defined) return Corr{make_float2(NAN, NAN), -1};
-    const double* C = sf.c[s];
+__device__ __forceinline__ double pooled_at(const uint8_t* frame, int Wd, int i, int j, int p) {
+    if constexpr (P == 1) {
+        const uint32_t off = ((uint32_t)i * (uint32_t)Wd + (uint32_t)j) * 4u;
+        return (double)*reinterpret_cast<const float*>(frame + off);
+    } else if constexpr (P == 2) {
+        const uint32_t off = ((uint32_t)(2 * i) * (uint32_t)Wd + (uint32_t)(2 * j)) * 4u;
+        const float2 r0 = *reinterpret_cast<const float2*>(frame + off);
+        const float2 r1 = *reinterpret_cast<const float2*>(frame + (off + (uint32_t)Wd * 4u));
+        return ((((double)r0.x + (double)r0.y) + (double)r1.x) + (double)r1.y) * 0.25;  // == / 4
+    } else {
+        return pooled<0>(reinterpret_cast<const float*>(frame), Wd, i, j, p);
+    }
+}
+
+// Eq. reprojection and Eq. visibility for one (lifted token, source frame).
+// Every lane evaluates the whole expression and the rejection causes pick
+// the result by selects, so a wave that mixes accepted and rejected tokens
+// takes no divergent branch; a rejected lane's values are discarded. Both
+// coordinates of u^ share one reciprocal of [X_s]_z when kShared.
+// floor(u^) is a truncation on the grid (u^ >= 0).
+template <int P, bool kShared>
+__device__ __forceinline__ Corr correspond(const ReprojectArgs& a, const Lifted& L, const double* C,
+                                           const uint8_t* frame, int Wd, int p, double tol) {
     // R_t X_t + c_t - c_s
     const double W0 = L.W[0] - C[9];
     const double W1 = L.W[1] - C[10];
@@ -131,16 +193,46 @@ __device__ __forceinline__ Corr correspond(const ReprojectArgs& a, const Lifted&
     const double Xs = (C[0] * W0 + C[3] * W1) + C[6] * W2;
     const double Ys = (C[1] * W0 + C[4] * W1) + C[7] * W2;
     const double Zs = (C[2] * W0 + C[5] * W1) + C[8] * W2;
-    if (!(Zs > 0.0)) return Corr{make_float2(NAN, NAN), -2};
-    const double fxs = C[12], fys = C[13], cxs = C[14], cys = C[15];
-    const double uhx = (fxs * Xs + cxs * Zs) / Zs;
-    const double uhy = (fys * Ys + cys * Zs) / Zs;
-    const float2 uv = make_float2((float)uhx, (float)uhy);
-    if (!(uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h)) return Corr{uv, -3};
-    const int kx = (int)floor(uhx);
-    const int ky = (int)floor(uhy);
-    const double Ds = pooled<P>(a.src_depth + (size_t)f * frame_px, Wd, ky, kx, p);
-    return Corr{uv, (Zs <= tol * Ds) ? ky * a.w + kx : -4};
+    const double hx = C[12] * Xs + C[14] * Zs;
+    const double hy = C[13] * Ys + C[15] * Zs;
+    double uhx, uhy;
+    if constexpr (kShared) {
+        const double y = 1.0 / Zs;
+        uhx = quotient_from_reciprocal(hx, Zs, y);
+        uhy = quotient_from_reciprocal(hy, Zs, y);
+    } else {
+        uhx = hx / Zs;
+        uhy = hy / Zs;
+    }
+    const bool front = L.defined && Zs > 0.0;
+    const bool on_grid = front && uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h;
+    const int kx = on_grid ? (int)uhx : 0;
+    const int ky = on_grid ? (int)uhy : 0;
+    const double Ds = pooled_at<P>(frame, Wd, ky, kx, p);
+    int code = on_grid ? ((Zs <= tol * Ds) ? ky * a.w + kx : -4) : -3;
+    code = front ? code : (L.defined ? -2 : -1);
+    const float2 uv = front ? make_float2((float)uhx, (float)uhy) : make_float2(NAN, NAN);
+    return Corr{uv, code};
+}
+
+// One token against sources s_begin .. s_end - 1: lift, then correspond and
+// store per source.
+template <int P, bool kShared>
+__device__ __forceinline__ void token_sources(const ReprojectArgs& a, const SrcFrames& sf, double z, int i, int j,
+                                              int b, int t, int tok, int s_begin, int s_end, int Lq, int hw, int Wd,
+                                              size_t frame_px, int p, double tol) {
+    const Lifted L = lift<kShared>(z, i, j, sf.tc, sf.trcp);
+    for (int s = s_begin; s < s_end; ++s) {
+        const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
+        const int f = __builtin_amdgcn_readfirstlane(sf.f[s]);
+        Corr c{make_float2(NAN, NAN), -5};
+        if (f >= 0) {
+            const uint8_t* frame = reinterpret_cast<const uint8_t*>(a.src_depth) + (size_t)f * frame_px * 4;
+            c = correspond<P, kShared>(a, L, sf.c[s], frame, Wd, p, tol);
+        }
+        st_uv(reinterpret_cast<float2*>(a.out_uv) + o, c.uv);
+        st_code(a.out_idx + o, c.code);
+    }
 }
 
 // kPerSource = false: a thread handles one token and loops over the S
@@ -174,42 +266,53 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
     const size_t frame_px = (size_t)hw * p * p;
     const int Lq = a.Tq * hw;
     const double pd = (double)p;
-
-    const float* Mt = a.tgt_c2w + (size_t)bt * 16;
-    const float* Kt = a.tgt_K + (size_t)bt * 4;
-    const double fxt = per_token<P>(Kt[0], pd), fyt = per_token<P>(Kt[1], pd);
-    const double cxt = per_token<P>(Kt[2], pd), cyt = per_token<P>(Kt[3], pd);
-    const Lifted L = lift<P>(pooled<P>(a.tgt_depth + (size_t)bt * frame_px, Wd, i, j, p), i, j, fxt, fyt, cxt, cyt, Mt);
+    const double z = pooled<P>(a.tgt_depth + (size_t)bt * frame_px, Wd, i, j, p);
     const double tol = 1.0 + a.eps;
 
-    // the problem's source frames (this block's one with kPerSource), converted once per block
+    // the target frame and the problem's source frames (this block's one with
+    // kPerSource), converted to doubles once per block, with the range check
+    // of the shared-reciprocal quotients
     __shared__ SrcFrames sf;
-    for (int s = s_begin + threadIdx.x; s < s_end; s += kBlock) {
+    const float* Mt = a.tgt_c2w + (size_t)bt * 16;
+    const float* Kt = a.tgt_K + (size_t)bt * 4;
+    int out_of_range = 0;
+    if (threadIdx.x < 16) {
+        const double x = frame_value<P>(Mt, Kt, threadIdx.x, pd);
+        sf.tc[threadIdx.x] = x;
+        out_of_range |= !frame_value_in_range(x, threadIdx.x);
+    } else if (threadIdx.x < 18) {
+        sf.trcp[threadIdx.x - 16] = 1.0 / frame_value<P>(Mt, Kt, threadIdx.x - 4, pd);
+    }
+    // one thread per (source, value)
+    for (int e = threadIdx.x; e < (s_end - s_begin) * 16; e += kBlock) {
+        const int s = s_begin + (e >> 4), v = e & 15;
         int f = b * a.S + s;
         if (a.src_sel) {
             f = a.src_sel[(size_t)b * a.S + s];
             if (f < 0 || f >= a.n_src) f = -1;
         }
-        sf.f[s] = f;
+        if (v == 0) sf.f[s] = f;
         if (f >= 0) {
-            const float* Ms = a.src_c2w + (size_t)f * 16;
-            const float* Ks = a.src_K + (size_t)f * 4;
-            for (int r = 0; r < 3; ++r) {
-                for (int c = 0; c < 3; ++c) sf.c[s][3 * r + c] = (double)Ms[4 * r + c];
-                sf.c[s][9 + r] = (double)Ms[4 * r + 3];
-            }
-            for (int c = 0; c < 4; ++c) sf.c[s][12 + c] = per_token<P>(Ks[c], pd);
+            const double x = frame_value<P>(a.src_c2w + (size_t)f * 16, a.src_K + (size_t)f * 4, v, pd);
+            sf.c[s][v] = x;
+            out_of_range |= !frame_value_in_range(x, v);
         }
     }
+    // one flag per wave (a ballot), read by every wave after the barrier
+    const int any_out = __any(out_of_range);
+    if ((threadIdx.x & 63) == 0) sf.out_of_range[threadIdx.x >> 6] = any_out;
     __syncthreads();
+    bool frames_in_range = true;
+#pragma unroll
+    for (int wv = 0; wv < kBlock / 64; ++wv) frames_in_range = frames_in_range && !sf.out_of_range[wv];
     if (tok >= hw) return;
-
-    for (int s = s_begin; s < s_end; ++s) {
-        const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
-        const Corr c = correspond<P>(a, L, sf, s, Wd, frame_px, p, tol);
-        st_uv(reinterpret_cast<float2*>(a.out_uv) + o, c.uv);
-        st_code(a.out_idx + o, c.code);
-    }
+    // a depth outside [2^-40, 2^40] sends its wave to the division path
+    // (undefined depths are rejected whatever the path computes for them)
+    const bool z_in_range = !(isfinite(z) && z > 0.0) || (z >= 0x1p-40 && z <= 0x1p40);
+    if (frames_in_range && __all(z_in_range))
+        token_sources<P, true>(a, sf, z, i, j, b, t, tok, s_begin, s_end, Lq, hw, Wd, frame_px, p, tol);
+    else
+        token_sources<P, false>(a, sf, z, i, j, b, t, tok, s_begin, s_end, Lq, hw, Wd, frame_px, p, tol);
 }
 
 // Rotation-only path (Sec. 4.3: with c_s = c_t the depth cancels in Eq.

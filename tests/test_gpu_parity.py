@@ -222,6 +222,29 @@ def test_reprojection_batched_and_no_source():
     assert (gidx[0, 2] == -5).all() and (gidx[1, 1] == -5).all() and (gidx[1, 3] == -5).all()
 
 
+def test_reprojection_outside_the_shared_reciprocal_range():
+    """The quotients of Eq. reprojection share one reciprocal of [X_s]_z only
+    where every frame value and the target depth lie in the range where that
+    equals IEEE division; elsewhere the kernel divides. Both paths, bit-exact
+    against the oracle: problem 0 in range; problem 1 with a band of target
+    depths at 1e-13 m and another at 1e13 m (defined, out of range: their waves
+    divide); problem 2 with a source centre 1e21 m away and problem 3 with a
+    source principal point of -0 (their blocks divide)."""
+    arrs = [a.copy() for a in W.make_reproj_batch(4, distinct=2)]
+    tgt_d, tgt_c, tgt_k, src_d, src_c, src_k = arrs
+    tgt_d[1, 0, 10:14, :] = 1e-13
+    tgt_d[1, 1, 30:34, :] = 1e13
+    src_c[2, 3, 0, 3] = 1e21
+    src_k[3, 4, 2] = -0.0
+    for B in (4, 1):
+        guv, gidx = rv.reproject_correspondence(*[dev(a[:B]) for a in arrs], p=2, eps=0.05)
+        guv, gidx = host(guv), host(gidx)
+        for b in range(B):
+            ouv, oidx = OR.reproject(*[a[b] for a in arrs], 2, 0.05)
+            _compare_reprojection(ouv, oidx, guv[b], gidx[b], 2, 30, 52, f"range case {b} (batch {B})")
+    assert (gidx[0] >= 0).mean() > 0.4
+
+
 def test_reprojection_per_token_and_per_source_launches_agree():
     """A launch of 32 problems runs one thread per token (looping over the
     sources); a launch of one problem, too small to fill the GPU that way,
