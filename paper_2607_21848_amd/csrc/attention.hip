@@ -442,8 +442,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         else return lds_r2;
     };
     __shared__ int lds_slot[kBias ? kMaxFramesLds : 1];        // KV frame -> retrieved frame (or -1)
-    __shared__ u32x4 lds_col[kBias ? kMaxGridSide : 1];        // key operand, first contraction half, by column
-    __shared__ u32x4 lds_row[kBias ? kMaxGridSide : 1];        // key operand, second contraction half, by row
+    // key operands by column (first contraction half, [0]) and by row (second half, [1])
+    __shared__ u32x4 lds_tab[2][kBias ? kMaxGridSide + 1 : 1];  // entry kMaxGridSide: zeros
     __shared__ float2 lds_corr[kBias ? kCorrLds : 1][128];      // centred u^ per (retrieved frame, query)
 
     const int tid = threadIdx.x;
@@ -519,6 +519,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             const int sv = a.slot[f];
             lds_slot[f] = (sv >= 0 && sv < a.S) ? sv : -1;
         }
+        if (tid < 2) lds_tab[tid][kMaxGridSide] = u32x4{0, 0, 0, 0};
         for (int i = tid; i < g.w + g.h; i += 256) {
             const bool col = i < g.w;
             const int k = col ? i : i - g.w;
@@ -527,8 +528,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             uint32_t ph, pm, pl;
             split3(-g.gamma * (ac * ac), ph, pm, pl);
             const u32x4 v = u32x4{pack2(a2, a2), pack2(a2, ph), pack2(pm, pl), col ? pack2(one_bf, one_bf) : one_bf};
-            if (col) lds_col[k] = v;
-            else lds_row[k] = v;
+            lds_tab[col ? 0 : 1][k] = v;
         }
     }
     const float inv_w = 1.0f / (float)g.w;
@@ -616,8 +616,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         }
         return as_bf16x8(v);
     };
-    // the operand of the frame the last biased tile lay in
-    int qcur_f = -1;
+    // query operand of the frame the last fast-path tile lay in (zeros for an unbiased frame)
     bf16x8 qcur = as_bf16x8(u32x4{0, 0, 0, 0});
     // slot of the frame the last fast-path tile lay in (uniform): looked up again only when the frame changes
     int scur_f = -1, scur = -1;
@@ -627,30 +626,44 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     auto key_operand = [&](int t) -> u32x4 {
         const int ky = (int)(((float)t + 0.5f) * inv_w);
         const int kx = t - ky * g.w;
-        return hh == 0 ? lds_col[kx] : lds_row[ky];
+        return lds_tab[hh][hh ? ky : kx];
+    };
+    // the same for a tile of frame slot s: zeros when the frame is not retrieved
+    auto key_operand_or_zero = [&](int t, int s) -> u32x4 {
+        const int ky = (int)(((float)t + 0.5f) * inv_w);
+        const int kx = t - ky * g.w;
+        return lds_tab[hh][s < 0 ? kMaxGridSide : (hh ? ky : kx)];
     };
 
-    // Bias of the QK tile starting at key k0, as the accumulator's start value.
-    // Fast path: the 32 keys lie in one frame -> one MFMA (or none for an
-    // unbiased frame). Slow path (a tile that crosses a frame boundary or Lk):
-    // one masked MFMA per retrieved frame the tile touches.
-    auto bias_init = [&](int k0) -> floatx16 {
-        floatx16 init = floatx16{0};
+    // Bias of the QK tile starting at key k0, as the accumulator's start value,
+    // in two parts. bias_classify runs early in a step, so that the key operand
+    // read from LDS lands before the bias MFMA needs it: it returns 1 for a
+    // tile inside one frame (the fast path; kop then holds the lane's key
+    // operand) and -1 for a tile that crosses a frame boundary or Lk.
+    // bias_init then issues one MFMA for a fast-path tile, with zero operands
+    // when the frame is not retrieved, so the common path has no branch; the
+    // frame's slot and query operand are looked up again only when the frame
+    // changes. A crossing tile takes one masked MFMA per retrieved frame it
+    // touches.
+    auto bias_classify = [&](int k0, u32x4& kop) -> int {
         const int span = min(31, Lk - 1 - k0);
-        if (span == 31 && blk_t + 31 < g.hw) {
-            if (scur_f != blk_f) {
+        if (__builtin_expect(span == 31 && blk_t + 31 < g.hw, 1)) {
+            if (__builtin_expect(scur_f != blk_f, 0)) {
                 scur = __builtin_amdgcn_readfirstlane(lds_slot[blk_f]);
                 scur_f = blk_f;
+                qcur = scur >= 0 ? query_operand(scur) : as_bf16x8(u32x4{0, 0, 0, 0});
             }
-            const int s = scur;
-            if (s >= 0) {
-                if (qcur_f != blk_f) {
-                    qcur = query_operand(s);
-                    qcur_f = blk_f;
-                }
-                init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(key_operand(blk_t + krow)), qcur, init, 0, 0, 0);
-            }
+            kop = key_operand_or_zero(blk_t + krow, scur);
+            return 1;
+        }
+        return -1;
+    };
+    auto bias_init = [&](int k0, int cls, const u32x4& kop) -> floatx16 {
+        floatx16 init = floatx16{0};
+        if (__builtin_expect(cls >= 0, 1)) {
+            init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), qcur, init, 0, 0, 0);
         } else {
+            const int span = min(31, Lk - 1 - k0);
             int lane_t = blk_t + krow, lane_f = blk_f;
             while (lane_t >= g.hw) {
                 lane_t -= g.hw;
@@ -677,7 +690,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // QK^T of one 32-key tile from LDS (buffer kt), bias first, into S
     auto qk_tile = [&](const uint8_t* kt, int k0, floatx16& S) {
         if constexpr (kBias) {
-            S = bias_init(k0);
+            u32x4 kop = u32x4{0, 0, 0, 0};
+            const int cls = bias_classify(k0, kop);
+            S = bias_init(k0, cls, kop);
         } else {
             S = floatx16{0};
         }
@@ -749,8 +764,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         if constexpr (kind <= 1)
             load_tile_lds(Vg, refill + kTileBytes + wave_off_v, (t0 + j + 2) * kTK, Lk, v_row_bytes, tlv, hd, wave, lane);
 
-        // K_{j+1} operands of the first QK MFMAs, read while the rescale check runs
+        // the bias operand of tile j + 1 first, then the K_{j+1} operands of the
+        // first QK MFMAs, read while the rescale check runs
         const int nk0 = (t0 + j + 1) * kTK;
+        u32x4 bias_kop = u32x4{0, 0, 0, 0};
+        int bias_cls = 0;
+        if constexpr (kBias && has_next) bias_cls = bias_classify(nk0, bias_kop);
         auto kread = [&](int i) -> u32x4 { return *reinterpret_cast<const u32x4*>(knext + koff[i]); };
         u32x4 kf[kKReads];
         if constexpr (has_next) {
@@ -771,7 +790,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             m_run = m_new;
         }
         if constexpr (has_next) {
-            if constexpr (kBias) S_next = bias_init(nk0);
+            if constexpr (kBias) S_next = bias_init(nk0, bias_cls, bias_kop);
             else S_next = floatx16{0};
         }
 
@@ -838,6 +857,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
+        // with the bias, keep the row-sum dot products of region A in it
+        // (otherwise they sink to the start of the next step, where they
+        // serialise behind the bias MFMA); without it they fit better there
+        if constexpr (kBias) asm volatile("" ::"v"(l_run0), "v"(l_run1));
         const bf16x8 pf0 = as_bf16x8(u32x4{w4[0][0], w4[0][1], w4[0][2], w4[0][3]});
 
         // region B1: PV of key half 0, softmax units (1, 2..3), V reads of key half 1
@@ -848,6 +871,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             vread(1, db);
             __builtin_amdgcn_sched_barrier(0);
         }
+        if constexpr (kBias) asm volatile("" ::"v"(l_run0), "v"(l_run1));
         const bf16x8 pf1 = as_bf16x8(u32x4{w4[1][0], w4[1][1], w4[1][2], w4[1][3]});
 
         // region B2: PV of key half 1, row maximum of tile j + 1 (keys past Lk
