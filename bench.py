@@ -117,6 +117,9 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device-to-device copy of this many MiB (5 times), the reference "
                          "kernel for scaling HBM byte counters")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the sweep over the five workload configurations (for profiler passes, which "
+                         "need only the headline stages)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: the benchmark runs on one GPU only (asked for --gpus {args.gpus}); the path would "
@@ -404,9 +407,11 @@ def main():
         f"Lk {int(np.median(s_lk))}, attention {stream_flops / (stream_ms * 1e-3) / 1e12:.1f} TFLOP/s over the chunk")
     del sq, sk, sv, so, slse, s_in
 
-    log("sweep over the five workload configurations")
-    configs = config_sweep(dev, stream, ws, q, k, v, slot, cuv, cidx, o, lse, wl, attn_ms, a8_ms, a8_dev,
-                           retr_ms, repr_ms, not args.no_cpu_baseline)
+    configs = None
+    if not args.no_configs:
+        log("sweep over the five workload configurations")
+        configs = config_sweep(dev, stream, ws, q, k, v, slot, cuv, cidx, o, lse, wl, attn_ms, a8_ms, a8_dev,
+                               retr_ms, repr_ms, not args.no_cpu_baseline)
 
     counters = profiled_counters()
     out = {
@@ -498,7 +503,8 @@ def main():
         },
     }
 
-    out["configs"] = configs
+    if configs is not None:
+        out["configs"] = configs
 
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
