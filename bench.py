@@ -509,16 +509,21 @@ def _timed(fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
-def _timed_rounds(fns, reps, stream, rounds=5):
+def _timed_rounds(fns, reps, stream, rounds=5, warm_s=0.1):
     """Median over `rounds` rounds of the mean milliseconds per call over `reps`
-    back-to-back calls, for each function of the dict `fns`. The functions take
-    turns round by round, so that they see the same clock and thermal state; a
-    single short burst right after other work can catch the clock in transition."""
+    back-to-back calls, for each function of the dict `fns`, after `warm_s`
+    seconds of untimed calls of each. The functions take turns round by round,
+    so that they see the same clock and thermal state. The GPU's clock settles
+    to a new load within tens of milliseconds: a short burst right after other
+    work (or after idling) measures the transition, not the kernel."""
     import torch
     res = {name: [] for name in fns}
     for fn in fns.values():
-        fn()
-        fn()
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < warm_s:
+            for _ in range(5):
+                fn()
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     for _ in range(rounds):
         for name, fn in fns.items():
