@@ -31,6 +31,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "internal.h"
 #include "quotient.h"
 
@@ -323,14 +325,42 @@ __global__ __launch_bounds__(kBlock) void reproject_kernel(ReprojectArgs a) {
 //     M = rows (fx_s A0 + cx_s A2, fy_s A1 + cy_s A2, A2)
 //     H[r] = (M[r][0] / fx_t, M[r][1] / fy_t, (M[r][2] - H[r][0] cx_t) - H[r][1] cy_t)
 // and each thread evaluates v = H u~ for two adjacent tokens, so the launch
-// is a pure write stream of 12 bytes per (token, source). The pair's u^ go
+// is a pure write stream of 12 bytes per (token, source). Where H is in the
+// shared-reciprocal range (homography_in_range), u^ = (v_0 / v_2, v_1 / v_2)
+// share one reciprocal of v_2 (quotient.h): the IEEE quotients there. The pair's u^ go
 // out as one 16-byte store and its codes as one 8-byte store where the pair
 // is aligned (an even element index in outputs whose base addresses are 16-
 // and 8-byte aligned: the common case), else one token at a time.
 struct SrcHomographies {
     double H[kMaxSrcLds][9];
     int status[kMaxSrcLds];  // 0 = use H, else the code of every token (-5, -6)
+    int shared[kMaxSrcLds];  // 1: H is in the shared-reciprocal range
 };
+
+// Range condition of the shared-reciprocal quotients (quotient.h) for a
+// homography: every entry zero or of magnitude in [2^-200, 2^200], and
+// neither numerator row (0, 1) all -0. Token centres are multiples of 1/2 in
+// [1/2, 2^28) (a frame holds at most 2^28 tokens), so every nonzero v_r is
+// a multiple of 2^-253 of magnitude below 2^230, the quotients lie in
+// [2^-483, 2^483] and their residuals are multiples of 2^-840: every
+// intermediate stays normal. A numerator is -0 only when its whole row is
+// -0 (the token centres are positive), which the condition excludes, so the
+// shared-reciprocal quotient is the IEEE one.
+__device__ __forceinline__ bool homography_in_range(const double* H) {
+    bool ok = true;
+#pragma unroll
+    for (int e = 0; e < 9; ++e) {
+        const double m = fabs(H[e]);
+        ok = ok && (H[e] == 0.0 || (m >= 0x1p-200 && m <= 0x1p200));
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const bool neg_zero_row = H[3 * r] == 0.0 && signbit(H[3 * r]) && H[3 * r + 1] == 0.0 &&
+                                  signbit(H[3 * r + 1]) && H[3 * r + 2] == 0.0 && signbit(H[3 * r + 2]);
+        ok = ok && !neg_zero_row;
+    }
+    return ok;
+}
 
 template <int P>
 __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
@@ -353,7 +383,7 @@ __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
             f = a.src_sel[(size_t)b * a.S + s];
             if (f < 0 || f >= a.n_src) f = -1;
         }
-        int status = 0;
+        int status = 0, shared = 0;
         if (f < 0) {
             status = -5;
         } else {
@@ -381,16 +411,20 @@ __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
                     A[1][c] = m1;
                     A[2][c] = m2;
                 }
+                double Hs[9];
                 for (int r = 0; r < 3; ++r) {
                     const double h0 = A[r][0] / fxt;
                     const double h1 = A[r][1] / fyt;
-                    sh.H[s][3 * r + 0] = h0;
-                    sh.H[s][3 * r + 1] = h1;
-                    sh.H[s][3 * r + 2] = (A[r][2] - h0 * cxt) - h1 * cyt;
+                    Hs[3 * r + 0] = h0;
+                    Hs[3 * r + 1] = h1;
+                    Hs[3 * r + 2] = (A[r][2] - h0 * cxt) - h1 * cyt;
                 }
+                for (int e = 0; e < 9; ++e) sh.H[s][e] = Hs[e];
+                shared = homography_in_range(Hs);
             }
         }
         sh.status[s] = status;
+        sh.shared[s] = shared;
     }
     __syncthreads();
     if (tok >= hw) return;
@@ -408,7 +442,10 @@ __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
         const size_t o = ((size_t)b * a.S + s) * Lq + (size_t)t * hw + tok;
         float2 uv[2] = {make_float2(NAN, NAN), make_float2(NAN, NAN)};
         int code[2] = {sh.status[s], sh.status[s]};
-        if (code[0] == 0) {
+        // both tokens of the pair, with one reciprocal of v_2 per token in the
+        // shared-reciprocal range (kShared), else two divisions
+        auto evaluate = [&](auto shared_tag) {
+            constexpr bool kShared = decltype(shared_tag)::value;
             const double* H = sh.H[s];
 #pragma unroll
             for (int g = 0; g < 2; ++g) {
@@ -419,14 +456,25 @@ __global__ __launch_bounds__(kBlock) void rotation_kernel(ReprojectArgs a) {
                 if (!(v2 > 0.0)) {
                     code[g] = -2;
                 } else {
-                    const double uhx = v0 / v2;
-                    const double uhy = v1 / v2;
+                    double uhx, uhy;
+                    if constexpr (kShared) {
+                        const double y = 1.0 / v2;
+                        uhx = quotient_from_reciprocal(v0, v2, y);
+                        uhy = quotient_from_reciprocal(v1, v2, y);
+                    } else {
+                        uhx = v0 / v2;
+                        uhy = v1 / v2;
+                    }
                     uv[g] = make_float2((float)uhx, (float)uhy);
                     code[g] = (uhx >= 0.0 && uhx < (double)a.w && uhy >= 0.0 && uhy < (double)a.h)
                                   ? (int)floor(uhy) * a.w + (int)floor(uhx)
                                   : -3;
                 }
             }
+        };
+        if (code[0] == 0) {
+            if (sh.shared[s]) evaluate(std::true_type{});
+            else evaluate(std::false_type{});
         }
         if (two && a.paired && (o & 1) == 0) {
             f4 v = {uv[0].x, uv[0].y, uv[1].x, uv[1].y};

@@ -6,8 +6,10 @@ Cases: the panorama-clip workload at the 30 x 52 grid; ragged grids at
 p = 1, 2, 3 spanning several 128-token blocks with a partial last one; a
 source with a moved centre (code -6); a frame bank with empty and
 out-of-range selections (-5); the full 1024-problem launch the benchmark
-times, checked on sampled problems; S = 64 sources; and agreement with the general kernel
-(reproject_correspondence) on shared-centre inputs, where depth cancels.
+times, checked on sampled problems; S = 64 sources; agreement with the general kernel
+(reproject_correspondence) on shared-centre inputs, where depth cancels; and
+homographies outside the range where one shared reciprocal of v_2 gives the
+IEEE quotients (those pairs divide).
 """
 
 from __future__ import annotations
@@ -136,3 +138,25 @@ def test_rotation_maximum_source_count():
         wu, wi = R.reproject_rotation(tc[b], tk[b], sc[b], sk[b], 5, 7, 2)
         _check(uv[b], idx[b], wu, wi)
     assert (idx >= 0).any()
+
+
+def test_rotation_outside_the_shared_reciprocal_range():
+    """A (target, source) pair's two quotients share one reciprocal of v_2 only
+    where every entry of its homography lies in [2^-200, 2^200] (or is 0);
+    elsewhere the kernel divides. Both paths, bit-exact against the oracle in
+    one launch: problem 0 in range; in problem 1, target frame 0 has f_x =
+    1e-35 and source 2 f_x = 1e35 (entries near 2^232: that pair divides,
+    while target 0 with the other sources stays in range); in problem 2,
+    target frame 1 has f_y = 2e-38 and source 3 f_y = 1e37 (the same in y)."""
+    tc, tk, sc, sk = (a.copy() for a in W.make_rotation_batch(3, seed=91))
+    tk[1, 0, 0] = np.float32(1e-35)
+    sk[1, 2, 0] = np.float32(1e35)
+    tk[2, 1, 1] = np.float32(2e-38)
+    sk[2, 3, 1] = np.float32(1e37)
+    print("reproject_rotation: homographies outside the shared-reciprocal range", flush=True)
+    uv, idx = rv.reproject_rotation(_d(tc), _d(tk), _d(sc), _d(sk), h=30, w=52, p=2)
+    uv, idx = uv.cpu().numpy(), idx.cpu().numpy()
+    for b in range(3):
+        wu, wi = R.reproject_rotation(tc[b], tk[b], sc[b], sk[b], 30, 52, 2)
+        _check(uv[b], idx[b], wu, wi)
+    assert (idx[0] >= 0).mean() > 0.3
