@@ -392,12 +392,13 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(const lds_void*)p;
 }
 
-// lds_wave: LDS byte address of this wave's quarter of the destination tile (uniform)
-template <class Fmt>
-__device__ __forceinline__ void load_tile_lds(const uint8_t* __restrict__ src, uint32_t lds_wave, int tile0, int Lk,
-                                              size_t row_bytes, const TileLoad<Fmt>& tl, int hd, int wave, int lane) {
-    const uint8_t* base = src + (size_t)tile0 * row_bytes;
-    if (tile0 + kTK <= Lk) {
+// lds_wave: LDS byte address of this wave's quarter of the destination tile
+// (uniform); base: the tile's first row (tile0 of the key range). kFull: the
+// caller knows the tile lies inside Lk (every tile but the range's last).
+template <class Fmt, bool kFull = false>
+__device__ __forceinline__ void load_tile_at(const uint8_t* __restrict__ base, uint32_t lds_wave, int tile0, int Lk,
+                                             size_t row_bytes, const TileLoad<Fmt>& tl, int hd, int wave, int lane) {
+    if (kFull || tile0 + kTK <= Lk) {
 #pragma unroll
         for (int i = 0; i < Fmt::kLoads; ++i) dma_b128(base, tl.off[i], lds_wave + i * 1024);
     } else {
@@ -410,6 +411,11 @@ __device__ __forceinline__ void load_tile_lds(const uint8_t* __restrict__ src, u
             dma_b128(base, off, lds_wave + i * 1024);
         }
     }
+}
+template <class Fmt>
+__device__ __forceinline__ void load_tile_lds(const uint8_t* __restrict__ src, uint32_t lds_wave, int tile0, int Lk,
+                                              size_t row_bytes, const TileLoad<Fmt>& tl, int hd, int wave, int lane) {
+    load_tile_at<Fmt>(src + (size_t)tile0 * row_bytes, lds_wave, tile0, Lk, row_bytes, tl, hd, wave, lane);
 }
 
 // Workgroup barrier with no memory fence. __syncthreads() would also drain
@@ -548,6 +554,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     load_tile_lds(Kg, kdst(R1{}), tile1, Lk, qk_row_bytes, tlk, hd, wave, lane);
     load_tile_lds(Vg, vdst(R2{}), tile1, Lk, v_row_bytes, tlv, hd, wave, lane);
     load_tile_lds(Kg, kdst(R2{}), tile2, Lk, qk_row_bytes, tlk, hd, wave, lane);
+    // the loads of the steps: K_{j+3} and V_{j+2} at step j, through pointers
+    // that advance one tile per step (no per-step 64-bit multiply)
+    const size_t k_stride = (size_t)kTK * qk_row_bytes, v_stride = (size_t)kTK * v_row_bytes;
+    const uint8_t* k_load = Kg + (size_t)(t0 + 3) * k_stride;
+    const uint8_t* v_load = Vg + (size_t)(t0 + 2) * v_stride;
 
     // Q fragments: lane (hh, n) holds Q[q][16 kk + 8 hh .. +8)
     // (fp8: lane (hh, n) holds Q[q][64 kk + 32 hh .. +32), kk = 0, 1)
@@ -632,7 +643,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     auto key_operand_or_zero = [&](int t, int s) -> u32x4 {
         const int ky = (int)(((float)t + 0.5f) * inv_w);
         const int kx = t - ky * g.w;
-        return lds_tab[hh][s < 0 ? kMaxGridSide : (hh ? ky : kx)];
+        const int none = s >> 31;  // all ones when the frame is not retrieved (no branch)
+        return lds_tab[hh][((hh ? ky : kx) & ~none) | (kMaxGridSide & none)];
     };
 
     // Bias of the QK tile starting at key k0, as the accumulator's start value,
@@ -645,9 +657,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // frame's slot and query operand are looked up again only when the frame
     // changes. A crossing tile takes one masked MFMA per retrieved frame it
     // touches.
-    auto bias_classify = [&](int k0, u32x4& kop) -> int {
-        const int span = min(31, Lk - 1 - k0);
-        if (__builtin_expect(span == 31 && blk_t + 31 < g.hw, 1)) {
+    auto bias_classify = [&](auto inside_tag, int k0, u32x4& kop) -> int {
+        constexpr bool kInside = decltype(inside_tag)::value;  // the tile is known to lie inside Lk
+        const bool inside = kInside || k0 + 31 < Lk;
+        if (__builtin_expect(inside && blk_t + 31 < g.hw, 1)) {
             if (__builtin_expect(scur_f != blk_f, 0)) {
                 scur = __builtin_amdgcn_readfirstlane(lds_slot[blk_f]);
                 scur_f = blk_f;
@@ -659,10 +672,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         return -1;
     };
     auto bias_init = [&](int k0, int cls, const u32x4& kop) -> floatx16 {
-        floatx16 init = floatx16{0};
-        if (__builtin_expect(cls >= 0, 1)) {
-            init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), qcur, init, 0, 0, 0);
-        } else {
+        // the fast path's MFMA, issued in every case so that the common path
+        // has no branch: kop is zero unless the tile took the fast path, so a
+        // crossing tile starts its walk from exact zeros
+        floatx16 init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), qcur, floatx16{0}, 0, 0, 0);
+        if (__builtin_expect(cls < 0, 0)) {
             const int span = min(31, Lk - 1 - k0);
             int lane_t = blk_t + krow, lane_f = blk_f;
             while (lane_t >= g.hw) {
@@ -680,9 +694,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             }
         }
         blk_t += 32;
-        while (blk_t >= g.hw) {
-            blk_t -= g.hw;
-            ++blk_f;
+        if (__builtin_expect(blk_t >= g.hw, 0)) {
+            do {
+                blk_t -= g.hw;
+                ++blk_f;
+            } while (blk_t >= g.hw);
         }
         return init;
     };
@@ -691,7 +707,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     auto qk_tile = [&](const uint8_t* kt, int k0, floatx16& S) {
         if constexpr (kBias) {
             u32x4 kop = u32x4{0, 0, 0, 0};
-            const int cls = bias_classify(k0, kop);
+            const int cls = bias_classify(std::false_type{}, k0, kop);
             S = bias_init(k0, cls, kop);
         } else {
             S = floatx16{0};
@@ -748,7 +764,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // last few steps.
     auto step_core = [&](auto kind_tag, int j, floatx16& S_cur, floatx16& S_next, const uint8_t* knext,
                          const uint32_t refill) __attribute__((always_inline)) {
-        constexpr int kind = decltype(kind_tag)::value;
+        // kind 4: a step of the steady loop (kind 0 whose tiles j + 1 .. j + 3
+        // all lie inside Lk and are not the range's last)
+        constexpr bool kSteady = decltype(kind_tag)::value == 4;
+        constexpr int kind = kSteady ? 0 : decltype(kind_tag)::value;
         constexpr bool has_next = kind != 3;
         const uint8_t* vcur = knext + kTileBytes;
         // this lane's loads issued in step j - 1: K_{j+2} if it exists, V_{j+1} if it exists
@@ -760,16 +779,23 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             __builtin_amdgcn_s_waitcnt(kWaitVm0);
         }
         wg_barrier();
-        if constexpr (kind == 0) load_tile_lds(Kg, refill + wave_off_k, (t0 + j + 3) * kTK, Lk, qk_row_bytes, tlk, hd, wave, lane);
-        if constexpr (kind <= 1)
-            load_tile_lds(Vg, refill + kTileBytes + wave_off_v, (t0 + j + 2) * kTK, Lk, v_row_bytes, tlv, hd, wave, lane);
+        if constexpr (kind == 0) {
+            load_tile_at<KFmt, kSteady>(k_load, refill + wave_off_k, (t0 + j + 3) * kTK, Lk, qk_row_bytes, tlk, hd, wave,
+                                        lane);
+            k_load += k_stride;
+        }
+        if constexpr (kind <= 1) {
+            load_tile_at<RowsBf16, kSteady>(v_load, refill + kTileBytes + wave_off_v, (t0 + j + 2) * kTK, Lk, v_row_bytes,
+                                            tlv, hd, wave, lane);
+            v_load += v_stride;
+        }
 
         // the bias operand of tile j + 1 first, then the K_{j+1} operands of the
         // first QK MFMAs, read while the rescale check runs
         const int nk0 = (t0 + j + 1) * kTK;
         u32x4 bias_kop = u32x4{0, 0, 0, 0};
         int bias_cls = 0;
-        if constexpr (kBias && has_next) bias_cls = bias_classify(nk0, bias_kop);
+        if constexpr (kBias && has_next) bias_cls = bias_classify(std::integral_constant<bool, kSteady>{}, nk0, bias_kop);
         auto kread = [&](int i) -> u32x4 { return *reinterpret_cast<const u32x4*>(knext + koff[i]); };
         u32x4 kf[kKReads];
         if constexpr (has_next) {
@@ -780,7 +806,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
 
         // row maximum of tile j (reduced during the previous step) and lazy rescale
         const float mx = half_swap_max(mx_cur) * c_log2;
-        if (__any(mx > m_run + kRescaleSlack)) {
+        if (__builtin_expect(__any(mx > m_run + kRescaleSlack), 0)) {
             const float m_new = fmaxf(m_run, mx);
             const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
             l_run0 *= alpha;
@@ -916,12 +942,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // three more after it
     int j = 0;
     for (; j + 9 <= nt; j += 6) {
-        step(I0{}, I0{}, j);
-        step(I1{}, I0{}, j + 1);
-        step(I2{}, I0{}, j + 2);
-        step(I3{}, I0{}, j + 3);
-        step(I4{}, I0{}, j + 4);
-        step(I5{}, I0{}, j + 5);
+        step(I0{}, I4{}, j);
+        step(I1{}, I4{}, j + 1);
+        step(I2{}, I4{}, j + 2);
+        step(I3{}, I4{}, j + 3);
+        step(I4{}, I4{}, j + 4);
+        step(I5{}, I4{}, j + 5);
     }
     // the last 1 .. 8 tiles: one copy of the step body per kind, ring slot
     // chosen at run time. The steady loop leaves off at a multiple of six, so

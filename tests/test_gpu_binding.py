@@ -92,3 +92,27 @@ def test_rotation_binding_checks_and_unbatched_form():
     assert torch.equal(uv1.view(torch.int32), uv[0].view(torch.int32))
     # identity poses: every token of each of the 3 frames maps onto itself
     assert torch.equal(idx[1, 0], torch.arange(117, dtype=torch.int32, device=DEV).repeat(3))
+
+
+def test_rotation_offset_output_views():
+    """reproject_rotation stores a token pair's u^ as one 16-byte store and its
+    codes as one 8-byte store only where those addresses are so aligned.
+    Outputs that start one element into larger buffers (u^ 8-byte but not
+    16-byte aligned, codes 4-byte but not 8-byte aligned) take single stores
+    and give the same bits as aligned outputs."""
+    import numpy as np
+    import workloads as W
+    tc, tk, sc, sk = (torch.from_numpy(np.ascontiguousarray(a)).to(DEV) for a in W.make_rotation_batch(3, seed=5))
+    kw = dict(h=30, w=52, p=2)
+    B, S, Lq = 3, 6, 3 * 30 * 52
+    print("reproject_rotation: offset output views", flush=True)
+    uv, idx = rv.reproject_rotation(tc, tk, sc, sk, **kw)
+    uv_buf = torch.full((B * S * Lq * 2 + 2,), 7.0, device=DEV)
+    idx_buf = torch.full((B * S * Lq + 1,), 7, dtype=torch.int32, device=DEV)
+    ouv, oidx = uv_buf[2:].view(B, S, Lq, 2), idx_buf[1:].view(B, S, Lq)
+    assert ouv.data_ptr() % 16 == 8 and oidx.data_ptr() % 8 == 4
+    rv.reproject_rotation(tc, tk, sc, sk, **kw, out=(ouv, oidx))
+    torch.cuda.synchronize()
+    assert torch.equal(oidx, idx)
+    assert torch.equal(ouv.view(torch.int32), uv.view(torch.int32))
+    assert uv_buf[:2].eq(7.0).all() and idx_buf[:1].eq(7).all()  # nothing written before the views
