@@ -742,6 +742,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
 #pragma unroll
     for (int db = 0; db < 4; ++db) O[db] = floatx16{0};
     float m_run = -INFINITY, l_run0 = 0.0f, l_run1 = 0.0f;
+    // a raw logit above this calls for a rescale: (m_run + kRescaleSlack) / c_log2,
+    // so the check needs neither the row's other half nor the scale
+    float m_thr = -INFINITY;
     const uint32_t ones2 = 0x3f803f80u;  // bf16 (1, 1)
     using True = std::integral_constant<bool, true>;
     using False = std::integral_constant<bool, false>;
@@ -804,9 +807,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             kf[2] = kread(2);
         }
 
-        // row maximum of tile j (reduced during the previous step) and lazy rescale
-        const float mx = half_swap_max(mx_cur) * c_log2;
-        if (__builtin_expect(__any(mx > m_run + kRescaleSlack), 0)) {
+        // lazy rescale: tested on each lane's half of the row maximum of tile j
+        // (reduced during the previous step); the whole row's maximum only when needed
+        if (__builtin_expect(__any(mx_cur > m_thr), 0)) {
+            const float mx = half_swap_max(mx_cur) * c_log2;
             const float m_new = fmaxf(m_run, mx);
             const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
             l_run0 *= alpha;
@@ -814,6 +818,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
 #pragma unroll
             for (int db = 0; db < 4; ++db) O[db] *= alpha;
             m_run = m_new;
+            m_thr = (m_run + kRescaleSlack) / c_log2;
         }
         if constexpr (has_next) {
             if constexpr (kBias) S_next = bias_init(nk0, bias_cls, bias_kop);
