@@ -647,16 +647,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         return lds_tab[hh][((hh ? ky : kx) & ~none) | (kMaxGridSide & none)];
     };
 
-    // Bias of the QK tile starting at key k0, as the accumulator's start value,
-    // in two parts. bias_classify runs early in a step, so that the key operand
-    // read from LDS lands before the bias MFMA needs it: it returns 1 for a
-    // tile inside one frame (the fast path; kop then holds the lane's key
-    // operand) and -1 for a tile that crosses a frame boundary or Lk.
-    // bias_init then issues one MFMA for a fast-path tile, with zero operands
-    // when the frame is not retrieved, so the common path has no branch; the
-    // frame's slot and query operand are looked up again only when the frame
-    // changes. A crossing tile takes one masked MFMA per retrieved frame it
-    // touches.
+    // Bias of the QK tile starting at key k0, added to its logits after the
+    // QK MFMAs, in two parts. bias_classify runs at the start of a step, so
+    // that the key operand read from LDS lands while the QK MFMAs run: it
+    // returns 1 for a tile inside one frame (the fast path; kop then holds
+    // the lane's key operand) and -1 for a tile that crosses a frame boundary
+    // or Lk. bias_add then issues one MFMA for a fast-path tile, with zero
+    // operands when the frame is not retrieved, so the common path has no
+    // branch; the frame's slot and query operand are looked up again only
+    // when the frame changes. A crossing tile adds one masked MFMA per
+    // retrieved frame it touches.
     auto bias_classify = [&](auto inside_tag, int k0, u32x4& kop) -> int {
         constexpr bool kInside = decltype(inside_tag)::value;  // the tile is known to lie inside Lk
         const bool inside = kInside || k0 + 31 < Lk;
@@ -671,11 +671,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         }
         return -1;
     };
-    auto bias_init = [&](int k0, int cls, const u32x4& kop) -> floatx16 {
+    // Adds the bias of the QK tile starting at key k0 to acc, its logits.
+    auto bias_add = [&](floatx16 init, int k0, int cls, const u32x4& kop) -> floatx16 {
         // the fast path's MFMA, issued in every case so that the common path
-        // has no branch: kop is zero unless the tile took the fast path, so a
-        // crossing tile starts its walk from exact zeros
-        floatx16 init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), qcur, floatx16{0}, 0, 0, 0);
+        // has no branch: kop is zero unless the tile took the fast path (it
+        // then adds exact zeros), and a crossing tile adds its frames after it
+        init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), qcur, init, 0, 0, 0);
         if (__builtin_expect(cls < 0, 0)) {
             const int span = min(31, Lk - 1 - k0);
             int lane_t = blk_t + krow, lane_f = blk_f;
@@ -703,15 +704,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         return init;
     };
 
-    // QK^T of one 32-key tile from LDS (buffer kt), bias first, into S
+    // QK^T of one 32-key tile from LDS (buffer kt) into S, then its bias
     auto qk_tile = [&](const uint8_t* kt, int k0, floatx16& S) {
-        if constexpr (kBias) {
-            u32x4 kop = u32x4{0, 0, 0, 0};
-            const int cls = bias_classify(std::false_type{}, k0, kop);
-            S = bias_init(k0, cls, kop);
-        } else {
-            S = floatx16{0};
-        }
+        u32x4 kop = u32x4{0, 0, 0, 0};
+        int cls = 0;
+        if constexpr (kBias) cls = bias_classify(std::false_type{}, k0, kop);
+        S = floatx16{0};
 #pragma unroll
         for (int kk = 0; kk < kQFrags; ++kk) {
             if constexpr (kFp8) {
@@ -723,6 +721,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
                 S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], S, 0, 0, 0);
             }
         }
+        if constexpr (kBias) S = bias_add(S, k0, cls, kop);
     };
     // mask keys past Lk (only the last tile can hold any) and reduce this lane's maximum
     auto tile_max = [&](auto mask_tag, floatx16& S, int k0) -> float {
@@ -796,9 +795,6 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         // the bias operand of tile j + 1 first, then the K_{j+1} operands of the
         // first QK MFMAs, read while the rescale check runs
         const int nk0 = (t0 + j + 1) * kTK;
-        u32x4 bias_kop = u32x4{0, 0, 0, 0};
-        int bias_cls = 0;
-        if constexpr (kBias && has_next) bias_cls = bias_classify(std::integral_constant<bool, kSteady>{}, nk0, bias_kop);
         auto kread = [&](int i) -> u32x4 { return *reinterpret_cast<const u32x4*>(knext + koff[i]); };
         u32x4 kf[kKReads];
         if constexpr (has_next) {
@@ -806,6 +802,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             kf[1] = kread(1);
             kf[2] = kread(2);
         }
+        // the bias of tile j + 1 is added after its QK MFMAs, so its key
+        // operand read has the whole QK chain to land
+        u32x4 bias_kop = u32x4{0, 0, 0, 0};
+        int bias_cls = 0;
+        if constexpr (kBias && has_next) bias_cls = bias_classify(std::integral_constant<bool, kSteady>{}, nk0, bias_kop);
 
         // lazy rescale: tested on each lane's half of the row maximum of tile j
         // (reduced during the previous step); the whole row's maximum only when needed
@@ -820,10 +821,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             m_run = m_new;
             m_thr = (m_run + kRescaleSlack) / c_log2;
         }
-        if constexpr (has_next) {
-            if constexpr (kBias) S_next = bias_init(nk0, bias_cls, bias_kop);
-            else S_next = floatx16{0};
-        }
+        if constexpr (has_next) S_next = floatx16{0};
 
         // The rest of the step is scheduled by hand: every chunk below ends in
         // a scheduling fence, and pairs matrix-core work with VALU work that
@@ -888,6 +886,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
+        if constexpr (kBias && has_next) {
+            S_next = bias_add(S_next, nk0, bias_cls, bias_kop);
+            __builtin_amdgcn_sched_barrier(0);
+        }
         // with the bias, keep the row-sum dot products of region A in it
         // (otherwise they sink to the start of the next step, where they
         // serialise behind the bias MFMA); without it they fit better there
@@ -918,7 +920,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
                         if (nk0 + 16 * (i >> 3) + 8 * hh + (i & 7) >= Lk) S_next[i] = -INFINITY;
                     }
                 }
-                if (db == 0) mx_next = max3(S_next[0], S_next[1], fmaxf(S_next[2], S_next[3]));
+                // v_max3 only (fmaxf would add canonicalising maxes of its operands)
+                if (db == 0) mx_next = max3(max3(S_next[0], S_next[1], S_next[2]), S_next[3], S_next[3]);
                 else mx_next = max3(mx_next, max3(S_next[4 * db], S_next[4 * db + 1], S_next[4 * db + 2]), S_next[4 * db + 3]);
             }
             __builtin_amdgcn_sched_barrier(0);
