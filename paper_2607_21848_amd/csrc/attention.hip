@@ -781,6 +781,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             __builtin_amdgcn_s_waitcnt(kWaitVm0);
         }
         wg_barrier();
+        // the K_{j+1} operands of the first QK MFMAs first (the chain waits on them),
+        // then the refill of slot j mod 3 (it has two steps to land)
+        const int nk0 = (t0 + j + 1) * kTK;
+        auto kread = [&](int i) -> u32x4 { return *reinterpret_cast<const u32x4*>(knext + koff[i]); };
+        u32x4 kf[kKReads];
+        if constexpr (has_next) {
+            kf[0] = kread(0);
+            kf[1] = kread(1);
+            kf[2] = kread(2);
+        }
         if constexpr (kind == 0) {
             load_tile_at<KFmt, kSteady>(k_load, refill + wave_off_k, (t0 + j + 3) * kTK, Lk, qk_row_bytes, tlk, hd, wave,
                                         lane);
@@ -792,16 +802,6 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             v_load += v_stride;
         }
 
-        // the bias operand of tile j + 1 first, then the K_{j+1} operands of the
-        // first QK MFMAs, read while the rescale check runs
-        const int nk0 = (t0 + j + 1) * kTK;
-        auto kread = [&](int i) -> u32x4 { return *reinterpret_cast<const u32x4*>(knext + koff[i]); };
-        u32x4 kf[kKReads];
-        if constexpr (has_next) {
-            kf[0] = kread(0);
-            kf[1] = kread(1);
-            kf[2] = kread(2);
-        }
         // the bias of tile j + 1 is added after its QK MFMAs, so its key
         // operand read has the whole QK chain to land
         u32x4 bias_kop = u32x4{0, 0, 0, 0};
