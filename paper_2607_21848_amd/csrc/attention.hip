@@ -449,7 +449,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     };
     __shared__ int lds_slot[kBias ? kMaxFramesLds : 1];        // KV frame -> retrieved frame (or -1)
     // key operands by column (first contraction half, [0]) and by row (second half, [1])
-    __shared__ u32x4 lds_tab[2][kBias ? kMaxGridSide + 1 : 1];  // entry kMaxGridSide: zeros
+    __shared__ u32x4 lds_tab[2][kBias ? kMaxGridSide : 1];
     __shared__ float2 lds_corr[kBias ? kCorrLds : 1][128];      // centred u^ per (retrieved frame, query)
 
     const int tid = threadIdx.x;
@@ -520,12 +520,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // ---- bias state -------------------------------------------------------
     const int n_frames = Lk / g.hw;
     const uint32_t one_bf = 0x3f80u;
+    // the slot table's loads are issued here and stored to LDS after the
+    // query and correspondence loads have been issued too
+    constexpr int kSlotsPerThread = kBias ? kMaxFramesLds / 256 : 1;
+    int slot_v[kSlotsPerThread];
     if (kBias) {
-        for (int f = tid; f < n_frames; f += 256) {
-            const int sv = a.slot[f];
-            lds_slot[f] = (sv >= 0 && sv < a.S) ? sv : -1;
+#pragma unroll
+        for (int i = 0; i < kSlotsPerThread; ++i) {
+            const int f = tid + 256 * i;
+            slot_v[i] = f < n_frames ? a.slot[f] : -1;
         }
-        if (tid < 2) lds_tab[tid][kMaxGridSide] = u32x4{0, 0, 0, 0};
         for (int i = tid; i < g.w + g.h; i += 256) {
             const bool col = i < g.w;
             const int k = col ? i : i - g.w;
@@ -585,20 +589,36 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
     // Correspondences of the 128 queries for the first kCorrLds
     // retrieved frames, staged into LDS (centred u^, NaN = rejected), so that
     // no global load sits in the key loop; frames beyond load on demand.
+    // Every load is issued before any is used, so the staging waits for one
+    // memory latency rather than two per entry.
     if (kBias) {
         const int n_s = min(a.S, kCorrLds);
-        for (int e = tid; e < n_s * 128; e += 256) {
-            const int s = e >> 7, qi = e & 127;
-            const int qq = qt * 128 + qi;
-            float2 v = make_float2(NAN, NAN);
-            if (qq < a.Lq) {
+        constexpr int kPerThread = kCorrLds * 128 / 256;
+        int cidx[kPerThread];
+        float2 cuv[kPerThread];
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) {
+            const int e = tid + 256 * i;
+            const int s = e >> 7, qq = qt * 128 + (e & 127);
+            cidx[i] = -1;
+            cuv[i] = make_float2(0.0f, 0.0f);
+            if (s < n_s && qq < a.Lq) {
                 const size_t o = (size_t)s * a.Lq + qq;
-                if (a.corr_idx[o] >= 0) {
-                    const float2 u = reinterpret_cast<const float2*>(a.corr_uv)[o];
-                    v = make_float2(u.x - g.cx, u.y - g.cy);
-                }
+                cidx[i] = a.corr_idx[o];
+                cuv[i] = reinterpret_cast<const float2*>(a.corr_uv)[o];
             }
-            lds_corr[s][qi] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < kSlotsPerThread; ++i) {
+            const int f = tid + 256 * i;
+            if (f < n_frames) lds_slot[f] = (slot_v[i] >= 0 && slot_v[i] < a.S) ? slot_v[i] : -1;
+        }
+#pragma unroll
+        for (int i = 0; i < kPerThread; ++i) {
+            const int e = tid + 256 * i;
+            const int s = e >> 7;
+            if (s < n_s)
+                lds_corr[s][e & 127] = cidx[i] >= 0 ? make_float2(cuv[i].x - g.cx, cuv[i].y - g.cy) : make_float2(NAN, NAN);
         }
     }
     // query-side bias operand of retrieved frame s for this lane's query
@@ -639,24 +659,19 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         const int kx = t - ky * g.w;
         return lds_tab[hh][hh ? ky : kx];
     };
-    // the same for a tile of frame slot s: zeros when the frame is not retrieved
-    auto key_operand_or_zero = [&](int t, int s) -> u32x4 {
-        const int ky = (int)(((float)t + 0.5f) * inv_w);
-        const int kx = t - ky * g.w;
-        const int none = s >> 31;  // all ones when the frame is not retrieved (no branch)
-        return lds_tab[hh][((hh ? ky : kx) & ~none) | (kMaxGridSide & none)];
-    };
 
     // Bias of the QK tile starting at key k0, added to its logits after the
     // QK MFMAs, in two parts. bias_classify runs at the start of a step, so
     // that the key operand read from LDS lands while the QK MFMAs run: it
-    // returns 1 for a tile inside one frame (the fast path; kop then holds
-    // the lane's key operand) and -1 for a tile that crosses a frame boundary
-    // or Lk. bias_add then issues one MFMA for a fast-path tile, with zero
-    // operands when the frame is not retrieved, so the common path has no
-    // branch; the frame's slot and query operand are looked up again only
-    // when the frame changes. A crossing tile adds one masked MFMA per
-    // retrieved frame it touches.
+    // returns 1 for a tile inside one retrieved frame (the fast path; kop then
+    // holds the lane's key operand), 0 for a tile inside a frame that is not
+    // retrieved (no bias) and -1 for a tile that crosses a frame boundary or
+    // Lk. bias_add then issues one MFMA for a fast-path tile and none for an
+    // unbiased one: a uniform branch costs less than an MFMA of zeros, whose
+    // energy counts, as the chip runs this kernel at its power limit. The
+    // frame's slot and query operand are looked up again only when the frame
+    // changes. A crossing tile adds one masked MFMA per retrieved frame it
+    // touches.
     auto bias_classify = [&](auto inside_tag, int k0, u32x4& kop) -> int {
         constexpr bool kInside = decltype(inside_tag)::value;  // the tile is known to lie inside Lk
         const bool inside = kInside || k0 + 31 < Lk;
@@ -666,17 +681,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
                 scur_f = blk_f;
                 qcur = scur >= 0 ? query_operand(scur) : as_bf16x8(u32x4{0, 0, 0, 0});
             }
-            kop = key_operand_or_zero(blk_t + krow, scur);
+            if (scur < 0) return 0;  // frame not retrieved: no bias
+            kop = key_operand(blk_t + krow);
             return 1;
         }
         return -1;
     };
     // Adds the bias of the QK tile starting at key k0 to acc, its logits.
     auto bias_add = [&](floatx16 init, int k0, int cls, const u32x4& kop) -> floatx16 {
-        // the fast path's MFMA, issued in every case so that the common path
-        // has no branch: kop is zero unless the tile took the fast path (it
-        // then adds exact zeros), and a crossing tile adds its frames after it
-        init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), qcur, init, 0, 0, 0);
+        // the fast path's MFMA; a crossing tile adds its frames instead
+        if (cls > 0) init = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), qcur, init, 0, 0, 0);
         if (__builtin_expect(cls < 0, 0)) {
             const int span = min(31, Lk - 1 - k0);
             int lane_t = blk_t + krow, lane_f = blk_f;
@@ -855,17 +869,19 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         };
         __builtin_amdgcn_sched_barrier(0);
 
+        // Region A: the QK MFMAs of tile j + 1 (K operands read ahead) and the
+        // V reads of key half 0, then the bias of tile j + 1, then softmax
+        // units (0, 0..3) and (1, 0..1) of tile j. No softmax work sits
+        // between the QK MFMAs: with two waves on each SIMD the other wave's
+        // VALU work runs beside this wave's MFMA chain, and this order
+        // measured faster than pairing each QK MFMA with a softmax unit.
         if constexpr (kFp8) {
-            // region A: the 2 fp8 QK MFMAs of tile j + 1 (64 cycles each), each
-            // carrying three softmax units; the second also the V reads of key half 0
 #pragma unroll
             for (int kk = 0; kk < 2; ++kk) {
                 if constexpr (has_next) {
                     if (kk == 0) kf[3] = kread(3);
                     S_next = mfma_fp8(join8(kf[2 * kk], kf[2 * kk + 1]), qf[kk], S_next);
                 }
-#pragma unroll
-                for (int u = 3 * kk; u < 3 * kk + 3; ++u) unit(u >> 2, u & 3);
                 if (kk == 1) {
 #pragma unroll
                     for (int db = 0; db < 4; ++db) vread(0, db);
@@ -873,15 +889,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
                 __builtin_amdgcn_sched_barrier(0);
             }
         } else {
-            // region A: the 8 QK MFMAs of tile j + 1 (K operands read three ahead),
-            // softmax units (0, 0..3) and (1, 0..1), V reads of key half 0
 #pragma unroll
             for (int kk = 0; kk < 8; ++kk) {
                 if constexpr (has_next) {
                     if (kk + 3 < 8) kf[kk + 3] = kread(kk + 3);
                     S_next = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[kk]), qf[kk], S_next, 0, 0, 0);
                 }
-                if (kk < 6) unit(kk >> 2, kk & 3);
                 if (kk >= 4) vread(0, kk - 4);
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -890,9 +903,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
             S_next = bias_add(S_next, nk0, bias_cls, bias_kop);
             __builtin_amdgcn_sched_barrier(0);
         }
-        // with the bias, keep the row-sum dot products of region A in it
-        // (otherwise they sink to the start of the next step, where they
-        // serialise behind the bias MFMA); without it they fit better there
+#pragma unroll
+        for (int u = 0; u < 6; ++u) unit(u >> 2, u & 3);
+        __builtin_amdgcn_sched_barrier(0);
+        // with the bias, keep the row sums of these units here (otherwise they
+        // sink to the start of the next step, where they serialise behind the
+        // bias MFMA); without it they fit better there
         if constexpr (kBias) asm volatile("" ::"v"(l_run0), "v"(l_run1));
         const bf16x8 pf0 = as_bf16x8(u32x4{w4[0][0], w4[0][1], w4[0][2], w4[0][3]});
 
