@@ -10,7 +10,9 @@ resident in HBM before the timed region.
 Prints one JSON line. ``value`` is the algorithmic attention throughput of
 the whole step (4 Lq Lk D H flops per step / step time). ``roofline``
 describes the dominant kernel (biased attention) from HIP events recorded on
-its launch stream; ``stages`` adds per-stage times, the reprojection
+its launch stream, with the socket power and GFX clock amd-smi reports while
+that kernel runs back to back (the chip runs it at its power limit, below
+the 2.4 GHz clock the published peaks assume); ``stages`` adds per-stage times, the reprojection
 throughput of a batched launch (1024 independent problems, > 2x the 256 MB
 last-level cache), retrieval latency, the retrieval bandwidth on a stress
 bank, and the cache packing of the step's retrieved chunks for all 30
@@ -46,6 +48,7 @@ if ROOT not in sys.path:
 METRIC = "biased-attention TFLOP/s + MFMA util; reprojection tokens/s (Wan-1.3B shape)"
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+PEAK_CLOCK_MHZ = 2400.0  # the clock the published peaks are quoted at
 FP32_PEAK_TFLOPS = 157.3  # MI355X fp32 (the fp32 attention kernel runs on the fp32 matrix cores)
 FP8_BF16_PEAK_TFLOPS = 2.0 / (1.0 / 5000.0 + 1.0 / 2500.0)  # half the flops at the fp8 peak, half at bf16
 BENCH_QUERY = 1  # query chunk n = 225: a full top-4 retrieval
@@ -216,6 +219,14 @@ def main():
 
     # sanity: the step produced a full retrieval and finite outputs
     assert int(rcount.item()) == r.k and torch.isfinite(o.float()).all()
+
+    # the chip's power and clock while the headline attention runs back to back
+    power = _power_state(lambda: rv.biased_chunk_attention(
+        q, k, v, slot, cuv[0], cidx[0], h=wl.h, w=wl.w, softmax_scale=wl.softmax_scale, lam=wl.lam,
+        sigma=wl.sigma, out=(o, lse), workspace=ws))
+    if power is not None:
+        log(f"sustained attention: socket power {power['socket_power_w']:.0f} W, "
+            f"GFX clock {power['gfx_clock_mhz']:.0f} MHz ({power['samples']} samples)")
 
     # fp8 logits: the same chunk with q and k in fp8 e4m3 (v, o bf16). Half the flops (Q K^T) run on the
     # fp8 matrix cores, half (P V) on bf16 ones: the time-weighted peak is 2 / (1/5000 + 1/2500) TFLOP/s
@@ -417,6 +428,11 @@ def main():
             "valu_busy_profiled": counters.get("valu_busy_fraction"),
             "flops_per_launch": flops,
             "avg_launch_ms": round(attn_ms, 4),
+            # the power limit, not the 2.4 GHz peak clock, sets the clock this kernel runs at
+            "sustained_power_state": None if power is None else {
+                **power, "peak_at_that_clock": round(BF16_PEAK_TFLOPS * power["gfx_clock_mhz"] / PEAK_CLOCK_MHZ, 1),
+                "frac_at_that_clock": round(attn_tflops * PEAK_CLOCK_MHZ / (BF16_PEAK_TFLOPS * power["gfx_clock_mhz"]), 4),
+            },
         },
         "stages": {
             "retrieval_us": round(retr_ms * 1e3, 2),
@@ -491,6 +507,48 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def _power_state(fn, secs=3.0, settle_s=0.6):
+    """Median socket power (W) and GFX clock (MHz, mean over the XCDs) that
+    amd-smi reports while fn runs back to back for `secs` seconds, the first
+    `settle_s` of them unsampled; None where amd-smi is not available."""
+    import re
+    import subprocess
+    import threading
+    import torch
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        t_start = time.perf_counter()
+        while not stop.is_set():
+            if time.perf_counter() - t_start < settle_s:
+                time.sleep(0.05)
+                continue
+            try:
+                txt = subprocess.run(["amd-smi", "metric", "-p", "-c", "-g", "0"], capture_output=True, text=True,
+                                     timeout=10).stdout
+            except (OSError, subprocess.SubprocessError):
+                return
+            pw = re.search(r"SOCKET_POWER:\s+([0-9.]+)\s*W", txt)
+            clk = [float(c) for c in re.findall(r"GFX_\d+:\s+CLK:\s+([0-9.]+)\s*MHz", txt)]
+            if pw and clk:
+                samples.append((float(pw.group(1)), sum(clk) / len(clk)))
+            time.sleep(0.4)
+
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < secs:
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=15)
+    if not samples:
+        return None
+    return {"socket_power_w": float(np.median([s[0] for s in samples])),
+            "gfx_clock_mhz": round(float(np.median([s[1] for s in samples])), 1), "samples": len(samples)}
 
 
 def _timed(fn, reps, stream):
