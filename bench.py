@@ -237,16 +237,9 @@ def main():
     def attn8():
         rv.biased_chunk_attention(q8, k8, v, slot, cuv[0], cidx[0], h=wl.h, w=wl.w, softmax_scale=wl.softmax_scale,
                                   lam=wl.lam, sigma=wl.sigma, out=(o8, lse8), workspace=ws)
-    for _ in range(3):
-        attn8()
-    e8a, e8b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e8a.record(stream)
-    for _ in range(args.steps):
-        attn8()
-    e8b.record(stream)
-    torch.cuda.synchronize()
-    a8_ms = e8a.elapsed_time(e8b) / args.steps
+    # median rounds after a sustained warm-up, as every stage below: a burst right
+    # after the headline steps catches the clock moving to the new load
+    a8_ms = _timed_rounds({"fp8": attn8}, args.steps, stream)["fp8"]
     a8_tflops = flops / (a8_ms * 1e-3) / 1e12
     a8_dev = float((o8.float() - o.float()).abs().max().item())
     log(f"attention with fp8 logits {a8_ms:.3f} ms = {a8_tflops:.1f} TFLOP/s; max |O_fp8 - O_bf16| = {a8_dev:.2e}")
