@@ -226,7 +226,8 @@ def main():
         sigma=wl.sigma, out=(o, lse), workspace=ws))
     if power is not None:
         log(f"sustained attention: socket power {power['socket_power_w']:.0f} W, "
-            f"GFX clock {power['gfx_clock_mhz']:.0f} MHz ({power['samples']} samples)")
+            f"GFX clock {power['gfx_clock_mhz']:.0f} MHz, hotspot {power.get('hotspot_c', float('nan')):.0f} C "
+            f"({power['samples']} samples)")
 
     # fp8 logits: the same chunk with q and k in fp8 e4m3 (v, o bf16). Half the flops (Q K^T) run on the
     # fp8 matrix cores, half (P V) on bf16 ones: the time-weighted peak is 2 / (1/5000 + 1/2500) TFLOP/s
@@ -503,9 +504,10 @@ def main():
 
 
 def _power_state(fn, secs=3.0, settle_s=0.6):
-    """Median socket power (W) and GFX clock (MHz, mean over the XCDs) that
-    amd-smi reports while fn runs back to back for `secs` seconds, the first
-    `settle_s` of them unsampled; None where amd-smi is not available."""
+    """Median socket power (W), GFX clock (MHz, mean over the XCDs) and
+    hotspot and HBM temperatures (°C) that amd-smi reports while fn runs back
+    to back for `secs` seconds, the first `settle_s` of them unsampled; None
+    where amd-smi is not available."""
     import re
     import subprocess
     import threading
@@ -519,14 +521,17 @@ def _power_state(fn, secs=3.0, settle_s=0.6):
                 time.sleep(0.05)
                 continue
             try:
-                txt = subprocess.run(["amd-smi", "metric", "-p", "-c", "-g", "0"], capture_output=True, text=True,
-                                     timeout=10).stdout
+                txt = subprocess.run(["amd-smi", "metric", "-p", "-c", "-t", "-g", "0"], capture_output=True,
+                                     text=True, timeout=10).stdout
             except (OSError, subprocess.SubprocessError):
                 return
             pw = re.search(r"SOCKET_POWER:\s+([0-9.]+)\s*W", txt)
             clk = [float(c) for c in re.findall(r"GFX_\d+:\s+CLK:\s+([0-9.]+)\s*MHz", txt)]
+            hot = re.search(r"HOTSPOT:\s+([0-9.]+)", txt)
+            mem = re.search(r"\bMEM:\s+([0-9.]+)", txt)
             if pw and clk:
-                samples.append((float(pw.group(1)), sum(clk) / len(clk)))
+                samples.append((float(pw.group(1)), sum(clk) / len(clk), float(hot.group(1)) if hot else float("nan"),
+                                float(mem.group(1)) if mem else float("nan")))
             time.sleep(0.4)
 
     th = threading.Thread(target=sampler, daemon=True)
@@ -540,8 +545,13 @@ def _power_state(fn, secs=3.0, settle_s=0.6):
     th.join(timeout=15)
     if not samples:
         return None
-    return {"socket_power_w": float(np.median([s[0] for s in samples])),
-            "gfx_clock_mhz": round(float(np.median([s[1] for s in samples])), 1), "samples": len(samples)}
+    med = lambda i: float(np.median([s[i] for s in samples]))
+    out = {"socket_power_w": med(0), "gfx_clock_mhz": round(med(1), 1), "samples": len(samples)}
+    if not math.isnan(med(2)):
+        out["hotspot_c"] = med(2)
+    if not math.isnan(med(3)):
+        out["hbm_c"] = med(3)
+    return out
 
 
 def _timed(fn, reps, stream):
