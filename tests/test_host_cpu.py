@@ -1,7 +1,8 @@
 """Host-side contracts that need no GPU.
 
 * bench.py refuses more than one GPU with a message and a non-zero status
-  before touching a device;
+  before touching a device, and reads the power state amd-smi prints (or
+  records none where amd-smi is missing);
 * the entry module exposes build() and smoke();
 * the product path never reaches the oracle: importing the package loads
   nothing from oracle/, and no package source refers to it;
@@ -25,6 +26,49 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120, cwd=ROOT)
     assert r.returncode == 2
     assert "one GPU" in r.stdout
+
+
+_SMI_TEXT = """GPU: 0
+    POWER:
+        SOCKET_POWER: 1350 W
+        GFX_VOLTAGE: N/A
+        MEM_VOLTAGE: N/A
+    CLOCK:
+        GFX_0:
+            CLK: 1800 MHz
+            MAX_CLK: 2400 MHz
+        GFX_1:
+            CLK: 1700 MHz
+            MAX_CLK: 2400 MHz
+        MEM_0:
+            CLK: 2000 MHz
+    TEMPERATURE:
+        EDGE: N/A
+        HOTSPOT: 60 °C
+        MEM: 45 °C
+"""
+
+
+def test_bench_power_state_reads_amd_smi(monkeypatch):
+    sys.path.insert(0, ROOT)
+    import bench
+    import torch
+
+    class Done:
+        stdout = _SMI_TEXT
+
+    monkeypatch.setattr(torch.cuda, "synchronize", lambda *a, **k: None)
+    monkeypatch.setattr(subprocess, "run", lambda *a, **k: Done())
+    ps = bench._power_state(lambda: None, secs=0.3, settle_s=0.0)
+    assert ps is not None and ps["samples"] >= 1
+    # the clock is the mean over the XCDs; MAX_CLK and the HBM clock are not read as XCD clocks
+    assert (ps["socket_power_w"], ps["gfx_clock_mhz"], ps["hotspot_c"], ps["hbm_c"]) == (1350.0, 1750.0, 60.0, 45.0)
+
+    def missing(*a, **k):
+        raise FileNotFoundError("amd-smi")
+
+    monkeypatch.setattr(subprocess, "run", missing)
+    assert bench._power_state(lambda: None, secs=0.2, settle_s=0.0) is None
 
 
 def test_entry_module_exposes_build_and_smoke():
