@@ -1064,6 +1064,7 @@ namespace {
 // of one item: thread t takes query t / 32 and head dims 4 (t % 32) .. +3, so
 // that each wave reads two whole 512-byte partial rows per load.
 constexpr int kMergeQueries = 8;
+constexpr int kMergeBatch = 8;  // parts merged from registers loaded up front
 
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttentionArgs a, KeySplit ks) {
     const int n_qt = (a.Lq + 127) / 128;
@@ -1075,15 +1076,41 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttentionArgs a, KeySpl
     if (q >= a.Lq) return;
     const float* base = ks.part + (size_t)item * ks.parts * kPartFloats;
     float M = -INFINITY;
-    for (int p = 0; p < ks.parts; ++p) M = fmaxf(M, base[(size_t)p * kPartFloats + 128 * kD + qi]);
     float L = 0.0f;
     float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    for (int p = 0; p < ks.parts; ++p) {
-        const float* P = base + (size_t)p * kPartFloats;
-        const float c = __builtin_amdgcn_exp2f(P[128 * kD + qi] - M);
-        L = fmaf(c, P[128 * kD + 128 + qi], L);
-        const float4 v = *reinterpret_cast<const float4*>(P + qi * kD + d);
+    auto add = [&](float m, float l, float4 v) {
+        const float c = __builtin_amdgcn_exp2f(m - M);
+        L = fmaf(c, l, L);
         acc = make_float4(fmaf(c, v.x, acc.x), fmaf(c, v.y, acc.y), fmaf(c, v.z, acc.z), fmaf(c, v.w, acc.w));
+    };
+    if (ks.parts <= kMergeBatch) {
+        // every part's loads issued before any is used: one memory latency,
+        // not two per part
+        float m[kMergeBatch], l[kMergeBatch];
+        float4 v[kMergeBatch];
+#pragma unroll
+        for (int p = 0; p < kMergeBatch; ++p) {
+            if (p < ks.parts) {
+                const float* P = base + (size_t)p * kPartFloats;
+                m[p] = P[128 * kD + qi];
+                l[p] = P[128 * kD + 128 + qi];
+                v[p] = *reinterpret_cast<const float4*>(P + qi * kD + d);
+            }
+        }
+#pragma unroll
+        for (int p = 0; p < kMergeBatch; ++p) {
+            if (p < ks.parts) M = fmaxf(M, m[p]);
+        }
+#pragma unroll
+        for (int p = 0; p < kMergeBatch; ++p) {
+            if (p < ks.parts) add(m[p], l[p], v[p]);
+        }
+    } else {
+        for (int p = 0; p < ks.parts; ++p) M = fmaxf(M, base[(size_t)p * kPartFloats + 128 * kD + qi]);
+        for (int p = 0; p < ks.parts; ++p) {
+            const float* P = base + (size_t)p * kPartFloats;
+            add(P[128 * kD + qi], P[128 * kD + 128 + qi], *reinterpret_cast<const float4*>(P + qi * kD + d));
+        }
     }
     const float inv = 1.0f / L;
     uint16_t* Og = static_cast<uint16_t*>(a.o) + (size_t)q * a.H * kD + (size_t)hd * kD + d;
