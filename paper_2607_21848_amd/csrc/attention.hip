@@ -216,12 +216,14 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttentionArgs a, BiasGeom
 // so a direct load has two steps to land and each lane waits only for its
 // loads of two steps back. The steady loop is unrolled over a period of six
 // (ring slot and current logit registers are then compile-time). Inside a
-// step the instruction order is fixed by hand with scheduling fences: each
-// QK MFMA carries one softmax unit and the K reads three MFMAs ahead, the
-// PV MFMAs carry the V transpose reads and the row maxima, so one wave keeps
-// the matrix cores and the VALU busy and the second wave of the SIMD fills
-// the gaps. Work units are mapped XCD-aware so the workgroups of one head
-// (and key range) share an L2.
+// step the instruction order is fixed by hand with scheduling fences: the
+// QK MFMAs run back to back with the K reads three MFMAs ahead, then the
+// bias MFMA and most of the softmax, then the PV MFMAs carrying the V
+// transpose reads, the last softmax units and the row maxima. The two waves
+// of a SIMD fill each other's gaps: one wave's softmax runs beside the
+// other's MFMA chain, which measured faster than one wave pairing every QK
+// MFMA with a softmax unit of its own. Work units are mapped XCD-aware so
+// the workgroups of one head (and key range) share an L2.
 //
 // Softmax. exp2 on the raw hardware instruction with scale * log2(e) folded
 // into one FMA, probabilities packed to bf16 pairwise and summed with bf16
