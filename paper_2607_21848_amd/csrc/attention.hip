@@ -840,8 +840,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttentionArgs a, Bias
         if constexpr (has_next) S_next = floatx16{0};
 
         // The rest of the step is scheduled by hand: every chunk below ends in
-        // a scheduling fence, and pairs matrix-core work with VALU work that
-        // does not depend on it, so that one wave keeps both units busy.
+        // a scheduling fence. Matrix-core and VALU work are grouped rather
+        // than paired within a wave, so that the other wave of the SIMD can
+        // run its VALU work beside this wave's MFMAs and the other way round.
         // softmax unit (t, e): probabilities of logits 8 t + 2 e and 8 t + 2 e + 1
         // of tile j, packed to bf16 and added to the running sums
         uint32_t w4[2][4];
