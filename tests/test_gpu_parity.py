@@ -585,3 +585,26 @@ def test_attention_beyond_staged_frames_and_widest_grid(dtype):
         err, lerr = np.abs(host(o) - Oo).max(), np.abs(host(lse) - Lo).max()
         print(f"{dtype} S={S} grid {h}x{w}: max|dO|={err:.3e} max|dLSE|={lerr:.3e}")
         assert err <= tol and lerr <= ltol
+
+
+@pytest.mark.parametrize("dtype,key_parts", [("f32", 0), ("bf16", 0), ("bf16", 4)])
+def test_attention_most_kv_frames(dtype, key_parts):
+    """1024 KV frames, the most the slot table holds, on a 2 x 2 token grid:
+    every 32-key tile then crosses eight frames, and the retrieved frames
+    (24 of them, past the 16 staged in LDS) include the first and the last."""
+    Lq, nf, H, h, w, S = 70, 1024, 2, 2, 2, 24
+    rng = np.random.default_rng(1024)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    tol, ltol = (F32_TOL, LSE_F32_TOL) if dtype == "f32" else (BF16_TOL, LSE_BF16_TOL)
+    q, k, v, _, uv, idx = _synthetic(rng, Lq, nf * h * w, H, 128, h, w, S, dtype)
+    slot = np.full(nf, -1, np.int32)
+    frames = np.concatenate([[0, nf - 1], rng.choice(np.arange(1, nf - 1), size=S - 2, replace=False)])
+    slot[frames] = rng.permutation(S)
+    o, lse = rv.biased_chunk_attention(dev(q, tdt), dev(k, tdt), dev(v, tdt), dev(slot), dev(uv), dev(idx), h=h, w=w,
+                                       softmax_scale=1.0 / math.sqrt(128), lam=1.0, sigma=1.0, key_parts=key_parts)
+    Oo, Lo = OA.biased_attention(q, k, v, slot, uv, idx, h, w, 1.0 / math.sqrt(128), 1.0, 1.0)
+    O0, _ = OA.biased_attention(q, k, v, slot, None, None, h, w, 1.0 / math.sqrt(128), 0.0, 1.0)
+    err, lerr = np.abs(host(o) - Oo).max(), np.abs(host(lse) - Lo).max()
+    print(f"{dtype} {nf} frames, key_parts={key_parts}: max|dO|={err:.3e} max|dLSE|={lerr:.3e} "
+          f"(bias moves O by {np.abs(Oo - O0).max():.2e})")
+    assert err <= tol and lerr <= ltol
