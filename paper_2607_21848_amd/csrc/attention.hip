@@ -39,10 +39,8 @@
 #include <stdint.h>
 
 #include <algorithm>
-#include <mutex>
-#include <new>
+#include <atomic>
 #include <type_traits>
-#include <vector>
 
 #include "internal.h"
 
@@ -1217,8 +1215,11 @@ size_t attention_bf16_workspace_bytes(const AttentionArgs& a, int32_t parts) {
 static __device__ __align__(256) float scratch[kAttentionScratchBytes / sizeof(float)];
 
 namespace {
-std::mutex g_scratch_mutex;
-std::vector<float*> g_scratch_ptr;  // by device; nullptr = not looked up yet
+// The device address of the array on each device, looked up on the first call
+// there and kept in a fixed table, so that the lookup allocates nothing. Two
+// threads that look it up at once store the same address.
+constexpr int kScratchDevices = 64;
+std::atomic<float*> g_scratch_ptr[kScratchDevices];  // by device; nullptr = not looked up yet
 }  // namespace
 
 hipError_t attention_scratch(float** ptr) {
@@ -1226,20 +1227,16 @@ hipError_t attention_scratch(float** ptr) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    std::lock_guard<std::mutex> lock(g_scratch_mutex);
-    // no C++ exception may leave the library's C entry points
-    try {
-        if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize(dev + 1, nullptr);
-    } catch (const std::bad_alloc&) {
-        return hipErrorOutOfMemory;
-    }
-    if (!g_scratch_ptr[dev]) {
-        void* p = nullptr;
-        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+    float* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        void* addr = nullptr;
+        e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
         if (e != hipSuccess) return e;
-        g_scratch_ptr[dev] = static_cast<float*>(p);
+        p = static_cast<float*>(addr);
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
     }
-    *ptr = g_scratch_ptr[dev];
+    *ptr = p;
     return hipSuccess;
 }
 
