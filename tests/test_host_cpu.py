@@ -1,8 +1,9 @@
 """Host-side contracts that need no GPU.
 
 * bench.py refuses more than one GPU with a message and a non-zero status
-  before touching a device, and reads the power state amd-smi prints (or
-  records none where amd-smi is missing);
+  before touching a device, reads the power state amd-smi prints (or
+  records none where amd-smi is missing), and builds every key of its
+  one-line JSON result (headline, roofline and CPU-baseline objects);
 * the entry module exposes build() and smoke();
 * the product path never reaches the oracle: importing the package loads
   nothing from oracle/, and no package source refers to it;
@@ -47,6 +48,27 @@ _SMI_TEXT = """GPU: 0
         HOTSPOT: 60 °C
         MEM: 45 °C
 """
+
+
+def test_bench_result_carries_every_key():
+    """The keys of the JSON line, found among the string keys of the dict
+    literals and subscript assignments that bench.py builds."""
+    import ast
+
+    tree = ast.parse(open(os.path.join(ROOT, "bench.py")).read())
+    keys = set()
+    for node in ast.walk(tree):
+        if isinstance(node, ast.Dict):
+            keys |= {k.value for k in node.keys if isinstance(k, ast.Constant) and isinstance(k.value, str)}
+        elif isinstance(node, ast.Subscript) and isinstance(node.ctx, ast.Store):
+            if isinstance(node.slice, ast.Constant) and isinstance(node.slice.value, str):
+                keys.add(node.slice.value)
+    headline = {"metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better", "scaling",
+                "vs_baseline", "dtype", "data", "config", "workload"}
+    roofline = {"roofline", "bound", "achieved", "peak", "frac", "traffic"}
+    baseline = {"cpu_baseline", "cores", "kind", "sample"}
+    missing = (headline | roofline | baseline) - keys
+    assert not missing, f"bench.py never builds {sorted(missing)}"
 
 
 def test_bench_power_state_reads_amd_smi(monkeypatch):
