@@ -442,7 +442,8 @@ int pool_token_depth(const float* depth, int32_t n_frames, int32_t h, int32_t w,
  *   5. the packed cache of every layer (pack_retrieved_kv; keys enter the
  *      ring with the embedding of position 4F + f, as the network produced
  *      them for the current role, and are re-rotated to their role's
- *      position);
+ *      position); the anchor's rows, the same from chunk 1 on, are packed
+ *      at chunk 1 only;
  *   6. biased attention (Eq. bias) of every layer over its packed cache,
  *      the retrieved frames carrying slots 0..F-1 when a chunk was retrieved.
  *

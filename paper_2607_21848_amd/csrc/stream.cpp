@@ -301,8 +301,11 @@ int rc_stream_step(rc_stream* s, const float* depth, const float* c2w, const flo
         if (st != REVISIT_OK) return st;
     }
 
-    // the packed cache: runs of consecutive positions in one call each; the current chunk unrotated
-    for (int i0 = 0; i0 < n_parts;) {
+    // the packed cache: runs of consecutive positions in one call each; the current chunk unrotated.
+    // From chunk 2 on, part 0 is the anchor at rows 0..T-1 and positions 0..F-1, exactly as the
+    // previous step packed it (chunk 0 never leaves ring slot 0 and nothing else writes those rows),
+    // so it is not packed again.
+    for (int i0 = n >= 2 ? 1 : 0; i0 < n_parts;) {
         int i1 = i0 + 1;
         while (i1 < n_parts && !parts[i1].current && !parts[i0].current && parts[i1].pos == parts[i1 - 1].pos + F) ++i1;
         st = pack_retrieved_kv(s->ring_k, s->ring_v, s->store_pos, C, s->part_slot + i0, i1 - i0, parts[i0].pos,
